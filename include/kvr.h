@@ -1,0 +1,197 @@
+/*
+ * kvr.h - budgeted in-place KV-cache repair on one MI355X (gfx950) GPU.
+ *
+ * The method (paper, Section 3 "Cache Repair as Budgeted Recomputation"):
+ * a context C of n tokens has been prefilled into a key/value cache K(C).  A
+ * contiguous, length-preserving edit turns C into C' (c_i = c'_i outside the
+ * half-open span S = [edit_start, edit_end)), so positions and rotary phases
+ * are unchanged.  Repair recomputes a position set P = S u A, where A holds K
+ * positions chosen downstream of the span, from C' layer by layer over the
+ * stale cache and leaves every other cache entry unchanged ("The repair
+ * interface").  Recomputing every position reproduces the full prefill
+ * K(C') (Eq. 1).
+ *
+ * The model is a Llama-style pre-norm decoder: RMSNorm, Q/K/V projections
+ * (optional bias), rotary embedding (rotate-half pairing, angle
+ * p * theta^(-2i/head_dim) at each token's absolute position p), causal
+ * grouped-query attention with scale 1/sqrt(head_dim), output projection,
+ * SwiGLU MLP, residual connections and a final RMSNorm.
+ *
+ * Conventions for every call
+ * - All calls return kvr_status; no C++ exception crosses this interface.
+ * - Pointers named d_* are device pointers (hipMalloc'd or equivalent) on the
+ *   context's device; h_* are host pointers.  The caller owns every buffer it
+ *   passes; the library never frees them.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).  GPU
+ *   work is enqueued on it and the call returns without waiting; outputs are
+ *   valid once the stream has reached that point.  Calls on one context use
+ *   the context's workspace and must be ordered (one stream, or synchronised
+ *   by the caller); one context per host thread.
+ * - Arguments are validated before anything is enqueued: on any status other
+ *   than KVR_OK or KVR_E_HIP, no GPU work was enqueued and no cache was
+ *   touched.  KVR_E_HIP means a HIP call failed after enqueueing began; cache
+ *   contents are then undefined.  kvr_last_error() describes the failure.
+ *
+ * Data layouts
+ * - Weights: dtype of kvr_dims.dtype (fp32 or bf16), row-major.  Linear
+ *   weights are [out_features][in_features]; norm gains and biases are
+ *   vectors.  All weight pointers must be 16-byte aligned.
+ * - KV cache of one document: [n_layers][2][n_kv_heads][n_cap][head_dim]
+ *   (index 0 = keys after rotary embedding, 1 = values), dtype of
+ *   kvr_dims.dtype, 16-byte aligned.  kvr_cache_bytes() gives its size.
+ * - Tokens: int32 ids in [0, vocab).
+ * - Hidden outputs: fp32 rows of d_model values = the final RMSNorm output.
+ */
+#ifndef KVR_H
+#define KVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KVR_OK = 0,
+    KVR_E_ARG = 1,          /* NULL pointer, bad dims, unsorted/duplicate positions ... */
+    KVR_E_RANGE = 2,        /* a size or position outside what the call allows */
+    KVR_E_UNSUPPORTED = 3,  /* a shape or dtype this build does not handle */
+    KVR_E_NOMEM = 4,        /* workspace allocation failed */
+    KVR_E_HIP = 5           /* a HIP runtime call or kernel launch failed */
+} kvr_status;
+
+typedef enum { KVR_F32 = 0, KVR_BF16 = 1 } kvr_dtype;
+
+/* Model and workspace dimensions.
+ * head_dim must be even and at most 128; n_heads a multiple of n_kv_heads.
+ * max_ctx bounds n_cap of every cache the context is used with (it sizes the
+ * rotary table); max_rows bounds the total number of repaired rows |P| summed
+ * over the documents of one kvr_repair call.  fp32 computes every step in
+ * fp32; bf16 keeps weights, cache and matrix operands in bf16 with fp32
+ * accumulation, fp32 softmax/RMSNorm and an fp32 residual stream. */
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+    int32_t qkv_bias;      /* 1: Q/K/V projections carry a bias */
+    float rms_eps;
+    double rope_theta;
+    int32_t max_ctx;
+    int32_t max_rows;
+    kvr_dtype dtype;
+} kvr_dims;
+
+/* Device pointers of one layer.  wq [n_heads*head_dim][d_model],
+ * wk/wv [n_kv_heads*head_dim][d_model], wo [d_model][n_heads*head_dim],
+ * w_gate/w_up [d_ffn][d_model], w_down [d_model][d_ffn], attn_norm/mlp_norm
+ * [d_model]; bq/bk/bv are NULL unless qkv_bias. */
+typedef struct {
+    const void *attn_norm, *wq, *wk, *wv, *bq, *bk, *bv, *wo;
+    const void *mlp_norm, *w_gate, *w_up, *w_down;
+} kvr_layer_weights;
+
+/* embed [vocab][d_model] and final_norm [d_model] on the device; `layers` is a
+ * HOST array of n_layers entries (copied by kvr_create). */
+typedef struct {
+    const void *embed, *final_norm;
+    const kvr_layer_weights *layers;
+} kvr_weights;
+
+typedef struct kvr_ctx kvr_ctx;
+
+/* Create a context on the current HIP device.  The weight pointers are
+ * borrowed (not copied) and must stay valid until kvr_destroy.  The context
+ * allocates its workspace (sized from max_rows, max_ctx and the model dims;
+ * kvr_workspace_bytes reports it) and a pinned host staging buffer.
+ * Errors: KVR_E_ARG (NULL/invalid dims or misaligned/missing weights),
+ * KVR_E_UNSUPPORTED, KVR_E_NOMEM, KVR_E_HIP.  On error *out is NULL and the
+ * message is available through kvr_last_error(NULL). */
+kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *weights, kvr_ctx **out);
+
+/* Release the workspace.  Waits for the context's outstanding work. NULL ok. */
+void kvr_destroy(kvr_ctx *ctx);
+
+/* Bytes of one document's cache: n_layers*2*n_kv_heads*n_cap*head_dim*elem. */
+size_t kvr_cache_bytes(const kvr_dims *dims, int32_t n_cap);
+
+/* Device bytes held by the context (workspace, rotary table, scratch). */
+size_t kvr_workspace_bytes(const kvr_ctx *ctx);
+
+/* Full prefill K(C) (Section 3, "Question Setting"): run the decoder over all
+ * n tokens of d_tokens, writing the keys/values of positions [0, n) of every
+ * layer into d_cache (slots >= n are not touched).  If d_hidden_out is not
+ * NULL it receives the final RMSNorm output of every position, [n][d_model]
+ * fp32.  1 <= n <= n_cap <= max_ctx. */
+kvr_status kvr_prefill(kvr_ctx *ctx, const int32_t *d_tokens, int32_t n, int32_t n_cap,
+                       void *d_cache, float *d_hidden_out, void *stream);
+
+/* One document of a repair call. */
+typedef struct {
+    void *d_cache;              /* stale cache K(C), updated in place */
+    int32_t n, n_cap;           /* context length and the cache's slot capacity */
+    const int32_t *d_tokens_new;/* the full edited context C' [n] (device) */
+    int32_t edit_start, edit_end; /* half-open span S, 0 <= start <= end <= n */
+    const int32_t *h_positions; /* A: strictly ascending, in [0, n), disjoint
+                                   from S (host; copied during the call) */
+    int32_t n_positions;
+    float *d_hidden_out;        /* [|P|][d_model] fp32 rows in ascending
+                                   position order, or NULL */
+} kvr_doc;
+
+/* Repair R(K(C), C', P) with P = [edit_start, edit_end) u h_positions for each
+ * document (paper Section 3, "The repair interface").  Layer by layer, the
+ * rows of P are recomputed from C' (their embeddings at layer 0, their own
+ * outputs of the previous layer above it); at each layer the fresh keys and
+ * values of all of P are written into the cache first, then every p in P
+ * attends over slots t <= p of its own document, fresh where t is in P and
+ * stale elsewhere.  Slots outside P are never written.  Upstream positions
+ * (< edit_start) are accepted (the full-position endpoint, Eq. 1, needs
+ * them); policies select only downstream positions (kvr_select).
+ * Documents are independent; they are batched into one pass per layer.
+ * A document with an empty span and no positions is a no-op.
+ * Errors: KVR_E_ARG (NULL pointers, unsorted/duplicate positions, positions
+ * inside the span), KVR_E_RANGE (span or position outside [0, n), n > n_cap,
+ * n_cap > max_ctx, sum of |P| > max_rows). */
+kvr_status kvr_repair(kvr_ctx *ctx, const kvr_doc *docs, int32_t n_docs, void *stream);
+
+typedef enum { KVR_EDIT_LOCAL = 0, KVR_RANDOM = 1 } kvr_policy;
+
+/* Host-only position selection (paper Table 1; no context, no device).
+ * The pool is D = [edit_end, n - 1).  EDIT_LOCAL returns the first
+ * min(K, |D|) positions of D.  RANDOM returns min(K, |D|) distinct positions
+ * drawn uniformly from D: a SplitMix64 generator (Steele, Lea and Flood,
+ * OOPSLA 2014) seeded with `seed` drives a partial Fisher-Yates shuffle of D
+ * in ascending order, j = i + next() mod (|D| - i) for i < K, and the first
+ * entries are returned sorted ascending.  h_out must hold K entries; *n_out
+ * receives the count.  Errors: KVR_E_ARG (NULL outputs, K < 0, bad policy),
+ * KVR_E_RANGE (n < 1 or not 0 <= edit_start <= edit_end <= n). */
+kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_start, int32_t edit_end,
+                      int32_t K, uint64_t seed, int32_t *h_out, int32_t *n_out);
+
+typedef enum { KVR_EPI_STORE = 0, KVR_EPI_ADD = 1, KVR_EPI_SWIGLU = 2 } kvr_epilogue;
+
+/* One projection of the decoder exactly as the prefill and repair passes run
+ * it (same kernel choice and launch configuration for this shape), exposed
+ * for kernel benchmarks and tests.  Y = X W^T with X [rows][in_features] and
+ * W [out_features][in_features], both in the context's dtype, row-major,
+ * 16-byte aligned:
+ *   KVR_EPI_STORE:  d_out fp32 [rows][out_features] = Y
+ *   KVR_EPI_ADD:    d_out fp32 [rows][out_features] += Y (the residual add)
+ *   KVR_EPI_SWIGLU: d_out (dtype) [rows][out_features] = silu(X W^T) * (X W2^T),
+ *                   the SwiGLU MLP input; d_w = gate, d_w2 = up.
+ * d_w2 must be NULL unless SWIGLU.  1 <= rows <= the context's row capacity
+ * (max(max_rows, min(max_ctx, 8192))).  Uses the context's split-K scratch,
+ * so it is ordered with the context's other calls.
+ * Errors: KVR_E_ARG (NULL/misaligned pointers, bad epilogue), KVR_E_RANGE. */
+kvr_status kvr_linear(kvr_ctx *ctx, kvr_epilogue epilogue, const void *d_x, int32_t rows, int32_t in_features,
+                      const void *d_w, const void *d_w2, int32_t out_features, void *d_out, void *stream);
+
+/* Text of the last failure on this context, or of the last failed
+ * kvr_create/kvr_select when ctx is NULL.  Never NULL; valid until the next
+ * call on the same context. */
+const char *kvr_last_error(const kvr_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVR_H */

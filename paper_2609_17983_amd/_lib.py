@@ -1,0 +1,154 @@
+"""ctypes binding of libkvr.so (include/kvr.h): the same calls, argument
+marshalling only.  Every step of prefill and repair runs in the library's HIP
+kernels; nothing here computes.
+
+Device buffers are passed as integer addresses (e.g. ``tensor.data_ptr()``)
+and streams as integer handles (e.g. ``torch.cuda.current_stream().cuda_stream``).
+Non-OK statuses raise KvrError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int, c_int32, c_size_t, c_uint64, c_void_p
+from typing import Optional, Sequence
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvr.so")
+
+KVR_OK, KVR_E_ARG, KVR_E_RANGE, KVR_E_UNSUPPORTED, KVR_E_NOMEM, KVR_E_HIP = range(6)
+KVR_F32, KVR_BF16 = 0, 1
+KVR_EDIT_LOCAL, KVR_RANDOM = 0, 1
+
+STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPORTED", 4: "KVR_E_NOMEM",
+                5: "KVR_E_HIP"}
+
+KVR_EPI_STORE, KVR_EPI_ADD, KVR_EPI_SWIGLU = 0, 1, 2
+
+EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
+            "kvr_select", "kvr_linear", "kvr_last_error")
+
+
+class KvrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class kvr_dims(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("n_kv_heads", c_int32),
+                ("head_dim", c_int32), ("d_ffn", c_int32), ("vocab", c_int32), ("qkv_bias", c_int32),
+                ("rms_eps", c_float), ("rope_theta", c_double), ("max_ctx", c_int32), ("max_rows", c_int32),
+                ("dtype", c_int)]
+
+
+class kvr_layer_weights(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "bq", "bk", "bv", "wo",
+                                        "mlp_norm", "w_gate", "w_up", "w_down")]
+
+
+class kvr_weights(ctypes.Structure):
+    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p), ("layers", POINTER(kvr_layer_weights))]
+
+
+class kvr_doc(ctypes.Structure):
+    _fields_ = [("d_cache", c_void_p), ("n", c_int32), ("n_cap", c_int32), ("d_tokens_new", c_void_p),
+                ("edit_start", c_int32), ("edit_end", c_int32), ("h_positions", POINTER(c_int32)),
+                ("n_positions", c_int32), ("d_hidden_out", c_void_p)]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libkvr.so from the package directory; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_17983_amd.build`")
+    try:  # share torch's HIP runtime when torch is present (same SONAME)
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.kvr_create.argtypes = [POINTER(kvr_dims), POINTER(kvr_weights), POINTER(c_void_p)]
+    lib.kvr_create.restype = c_int
+    lib.kvr_destroy.argtypes = [c_void_p]
+    lib.kvr_destroy.restype = None
+    lib.kvr_cache_bytes.argtypes = [POINTER(kvr_dims), c_int32]
+    lib.kvr_cache_bytes.restype = c_size_t
+    lib.kvr_workspace_bytes.argtypes = [c_void_p]
+    lib.kvr_workspace_bytes.restype = c_size_t
+    lib.kvr_prefill.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_void_p]
+    lib.kvr_prefill.restype = c_int
+    lib.kvr_repair.argtypes = [c_void_p, POINTER(kvr_doc), c_int32, c_void_p]
+    lib.kvr_repair.restype = c_int
+    lib.kvr_select.argtypes = [c_int, c_int32, c_int32, c_int32, c_int32, c_uint64, POINTER(c_int32), POINTER(c_int32)]
+    lib.kvr_select.restype = c_int
+    lib.kvr_linear.argtypes = [c_void_p, c_int, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
+                               c_void_p]
+    lib.kvr_linear.restype = c_int
+    lib.kvr_last_error.argtypes = [c_void_p]
+    lib.kvr_last_error.restype = c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int, ctx: Optional[int] = None) -> None:
+    if status != KVR_OK:
+        raise KvrError(status, kvr_last_error(ctx))
+
+
+def kvr_last_error(ctx: Optional[int] = None) -> str:
+    msg = load().kvr_last_error(ctx)
+    return msg.decode() if msg else ""
+
+
+def kvr_create(dims: kvr_dims, weights: kvr_weights) -> int:
+    out = c_void_p()
+    _check(load().kvr_create(ctypes.byref(dims), ctypes.byref(weights), ctypes.byref(out)))
+    return out.value
+
+
+def kvr_destroy(ctx: Optional[int]) -> None:
+    load().kvr_destroy(ctx)
+
+
+def kvr_cache_bytes(dims: kvr_dims, n_cap: int) -> int:
+    return load().kvr_cache_bytes(ctypes.byref(dims), n_cap)
+
+
+def kvr_workspace_bytes(ctx: int) -> int:
+    return load().kvr_workspace_bytes(ctx)
+
+
+def kvr_prefill(ctx: int, d_tokens: int, n: int, n_cap: int, d_cache: int, d_hidden_out: Optional[int] = None,
+                stream: Optional[int] = None) -> None:
+    _check(load().kvr_prefill(ctx, d_tokens, n, n_cap, d_cache, d_hidden_out, stream), ctx)
+
+
+def make_doc(d_cache: int, n: int, n_cap: int, d_tokens_new: int, edit_start: int, edit_end: int,
+             positions: Sequence[int], d_hidden_out: Optional[int] = None) -> kvr_doc:
+    """A kvr_doc; the position array is kept alive on the returned object."""
+    arr = (c_int32 * max(1, len(positions)))(*positions)
+    doc = kvr_doc(d_cache, n, n_cap, d_tokens_new, edit_start, edit_end,
+                  ctypes.cast(arr, POINTER(c_int32)), len(positions), d_hidden_out)
+    doc._positions = arr  # keep alive
+    return doc
+
+
+def kvr_repair(ctx: int, docs: Sequence[kvr_doc], stream: Optional[int] = None) -> None:
+    arr = (kvr_doc * max(1, len(docs)))(*docs)
+    _check(load().kvr_repair(ctx, arr, len(docs), stream), ctx)
+
+
+def kvr_linear(ctx: int, epilogue: int, d_x: int, rows: int, in_features: int, d_w: int, d_w2: Optional[int],
+               out_features: int, d_out: int, stream: Optional[int] = None) -> None:
+    _check(load().kvr_linear(ctx, epilogue, d_x, rows, in_features, d_w, d_w2, out_features, d_out, stream), ctx)
+
+
+def kvr_select(policy: int, n: int, edit_start: int, edit_end: int, K: int, seed: int = 0) -> list:
+    out = (c_int32 * max(1, K))()
+    cnt = c_int32(0)
+    _check(load().kvr_select(policy, n, edit_start, edit_end, K, seed & ((1 << 64) - 1), out, ctypes.byref(cnt)))
+    return list(out[:cnt.value])

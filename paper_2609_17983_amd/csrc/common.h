@@ -1,0 +1,119 @@
+// Internal declarations shared by the library's HIP sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvr {
+
+typedef uint16_t bf16_t;  // raw bf16 bits in memory
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// One repaired (or prefilled) row: its document, absolute position, and the row
+// index of its final hidden state inside the document's output buffer.
+struct RowInfo {
+    int32_t pos;
+    int32_t doc;
+    int32_t out;
+    int32_t pad;
+};
+
+// One document of a pass.
+struct DocInfo {
+    void *cache;            // [L][2][Hkv][n_cap][hd]
+    const int32_t *tokens;  // C' (device)
+    float *hidden_out;      // [rows][d] or null
+    int32_t n, n_cap;
+    int32_t row0, nrows;    // rows of this document in the pass's row table
+};
+
+// One attention work item: up to 16 consecutive rows of one document, one kv
+// head group, keys [k0, k1).  part < 0: the item covers all keys its rows need
+// and writes the normalised output; otherwise it writes split partials at slot
+// `part` of the partial buffer.
+struct AttnItem {
+    int32_t doc;
+    int32_t row0, nrows;
+    int32_t kvh;
+    int32_t k0, k1;
+    int32_t part;
+    int32_t pad;
+};
+
+// Combine step for rows whose keys were split over several items.
+struct CombineItem {
+    int32_t row0, nrows;  // rows of the block
+    int32_t kvh;
+    int32_t part0, nparts;  // consecutive partial slots
+    int32_t pad[3];
+};
+
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// A linear layer Y[r][n] = sum_k X[r][k] * W[n][k] whose weight is the
+// concatenation of up to three row blocks (Q, K, V), or for SWIGLU the pair
+// (gate, up) with output A[r][f] = silu(gate) * up.
+struct LinearArgs {
+    const void *x;        // [R][K] operand (bf16 or fp32), row stride ldx
+    int32_t ldx;
+    int32_t R, K, N;      // N: output columns (SWIGLU: number of features f)
+    const void *w[3];     // row blocks of W
+    int32_t seg_end[3];   // cumulative output-column boundaries of the blocks
+    void *out;            // STORE: float [R][ldo]; RESID: float [R][ldo] (+=);
+                          // SWIGLU: operand type [R][ldo]
+    int32_t ldo;
+    float *partial;       // split-K scratch
+    int32_t *counters;    // split-K tile counters (kept at zero between calls)
+};
+
+// ---- launchers (each enqueues on `stream`; return hipSuccess or the launch error)
+
+hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int R, const void *embed,
+                        int d, int vocab, float *H, hipStream_t s);
+hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, const float *H, const void *gain, int R, int d,
+                          float eps, void *X, int ldx, hipStream_t s);
+hipError_t launch_final_norm(bool bf16_gain, const float *H, const void *gain, const RowInfo *rows,
+                             const DocInfo *docs, int R, int d, float eps, hipStream_t s);
+hipError_t launch_rope_scatter(bool bf16, const float *qkv, const void *bq, const void *bk, const void *bv,
+                               const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq, int Hkv,
+                               int hd, const float *rope_cos, const float *rope_sin, void *Q, hipStream_t s);
+hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
+                                   int layer, int Hq, int Hkv, int hd, void *O, hipStream_t s);
+hipError_t launch_attention_mfma(const bf16_t *Q, const RowInfo *rows, const DocInfo *docs,
+                                 const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
+                                 float *part, bf16_t *O, hipStream_t s);
+hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
+                                    int Hkv, bf16_t *O, hipStream_t s);
+hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
+// Skinny MFMA path (R <= 64): split = cross-block split-K factor, nt = 16-row
+// weight tiles per wave (2 or 4).
+hipError_t launch_linear_skinny(int epi, const LinearArgs &a, int split, int nt, hipStream_t s);
+// Tiled MFMA path for many rows.
+hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
+
+// Attention item geometry shared by the planner and the kernels.
+constexpr int ATT_ROWS = 16;   // query positions per item
+constexpr int ATT_KT = 64;     // keys per LDS tile
+constexpr int ATT_HD = 128;    // head_dim of the MFMA attention kernel
+
+}  // namespace kvr

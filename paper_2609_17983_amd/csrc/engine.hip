@@ -1,0 +1,512 @@
+// Context, validation, planning and the layer-by-layer launch sequence behind
+// the kvr_* C interface.
+//
+// One pass runs the decoder over a set of rows (positions of one or more
+// documents) against those documents' caches: embedding gather, then per layer
+// RMSNorm -> QKV projection -> rotary embedding + scatter of the fresh K/V into
+// the cache -> causal attention over the cache -> output projection (+
+// residual) -> RMSNorm -> gate/up projection with SwiGLU -> down projection (+
+// residual), and a final RMSNorm into the caller's output rows.  Repair is one
+// pass over P = S u A (paper Section 3, "The repair interface"); prefill is a
+// pass (or consecutive chunks of passes) over all positions.
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/kvr.h"
+#include "common.h"
+
+using namespace kvr;
+
+namespace kvr {
+
+static thread_local std::string g_error;
+void set_global_error(const char *msg) { g_error = msg; }
+
+}  // namespace kvr
+
+struct kvr_ctx {
+    kvr_dims d{};
+    int device = 0;
+    bool bf16 = true;
+    bool force_simple = false;
+    std::vector<kvr_layer_weights> layers;
+    const void *embed = nullptr, *final_norm = nullptr;
+
+    int rows_cap = 0;  // rows per pass
+    int max_docs = 0;
+    int items_cap = 0, comb_cap = 0;
+
+    char *ws = nullptr;
+    size_t ws_bytes = 0;
+    float *H = nullptr, *QKV = nullptr;
+    void *Xn = nullptr, *Qb = nullptr, *Ob = nullptr, *Ab = nullptr;
+    float *rope_cos = nullptr, *rope_sin = nullptr;
+    float *skinny_part = nullptr;
+    size_t skinny_part_floats = 0;
+    int *counters = nullptr;
+    int n_counters = 0;
+    float *attn_part = nullptr;
+    size_t attn_part_floats = 0;
+    char *d_tables = nullptr;
+    size_t tables_bytes = 0;
+
+    char *h_stage = nullptr;
+    hipEvent_t stage_ev = nullptr;
+    bool stage_pending = false;
+
+    std::string err;
+};
+
+namespace {
+
+constexpr int PREFILL_CHUNK = 8192;
+constexpr size_t SKINNY_PART_BYTES = 64ull << 20;
+constexpr size_t ATTN_PART_BYTES = 64ull << 20;
+constexpr int N_COUNTERS = 1 << 16;
+constexpr int PART_ROW = ATT_HD + 4;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+kvr_status fail(kvr_ctx *c, kvr_status st, const std::string &msg) {
+    if (c) c->err = msg;
+    else kvr::set_global_error(msg.c_str());
+    return st;
+}
+
+kvr_status hip_fail(kvr_ctx *c, hipError_t e, const char *what) {
+    return fail(c, KVR_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        int cur = 0;
+        if (hipGetDevice(&cur) == hipSuccess && cur != dev && hipSetDevice(dev) == hipSuccess) prev = cur;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t elem_size(const kvr_dims &d) { return d.dtype == KVR_BF16 ? 2 : 4; }
+
+struct Tables {
+    std::vector<RowInfo> rows;
+    std::vector<DocInfo> docs;
+    std::vector<AttnItem> items;
+    std::vector<CombineItem> comb;
+};
+
+// Split the key ranges of the row blocks over work items: without splitting
+// when there are enough items to fill the GPU, otherwise in chunks of KS keys
+// (multiple of the 64-key tile) so that about `target` items exist.
+void plan_attention(const kvr_ctx *c, Tables &t) {
+    const int Hkv = c->d.n_kv_heads;
+    const int G = c->d.n_heads / Hkv;
+    struct Block { int doc, row0, nrows, kmax; };
+    std::vector<Block> blocks;
+    for (int di = 0; di < (int)t.docs.size(); ++di) {
+        const DocInfo &dc = t.docs[di];
+        for (int b = 0; b < dc.nrows; b += ATT_ROWS) {
+            const int nb = std::min(ATT_ROWS, dc.nrows - b);
+            blocks.push_back({di, dc.row0 + b, nb, t.rows[dc.row0 + b + nb - 1].pos + 1});
+        }
+    }
+    const int target = 1024;
+    long long total_keys = 0;
+    for (auto &b : blocks) total_keys += b.kmax;
+    int KS = 1 << 30;
+    const size_t slot_floats = (size_t)G * ATT_ROWS * PART_ROW;
+    const size_t max_slots = c->attn_part_floats / slot_floats;
+    if ((long long)blocks.size() * Hkv < target / 2) {
+        long long ks = (total_keys * Hkv + target - 1) / target;
+        ks = std::max<long long>(256, (ks + ATT_KT - 1) / ATT_KT * ATT_KT);
+        for (;; ks *= 2) {
+            size_t slots = 0, nitems = 0;
+            for (auto &b : blocks) {
+                const long long ns = (b.kmax + ks - 1) / ks;
+                nitems += (size_t)ns * Hkv;
+                if (ns > 1) slots += (size_t)ns * Hkv;
+            }
+            if (slots <= max_slots && nitems <= (size_t)c->items_cap) break;
+        }
+        KS = (int)std::min<long long>(ks, 1 << 30);
+    }
+    int next_slot = 0;
+    for (auto &b : blocks) {
+        const int ns = (b.kmax + KS - 1) / KS;
+        for (int g = 0; g < Hkv; ++g) {
+            if (ns <= 1) {
+                t.items.push_back({b.doc, b.row0, b.nrows, g, 0, b.kmax, -1, 0});
+                continue;
+            }
+            CombineItem ci{};
+            ci.row0 = b.row0; ci.nrows = b.nrows; ci.kvh = g; ci.part0 = next_slot; ci.nparts = ns;
+            t.comb.push_back(ci);
+            for (int s = 0; s < ns; ++s)
+                t.items.push_back({b.doc, b.row0, b.nrows, g, s * KS, std::min(b.kmax, (s + 1) * KS), next_slot + s, 0});
+            next_slot += ns;
+        }
+    }
+    // longest key ranges first, so that short items fill the tail
+    std::stable_sort(t.items.begin(), t.items.end(),
+                     [](const AttnItem &x, const AttnItem &y) { return (x.k1 - x.k0) > (y.k1 - y.k0); });
+}
+
+// Split factor of the skinny linear layer: about 1024 blocks, each wavefront
+// keeping at least 8 k-steps of 32, and the partial tiles within the scratch.
+int skinny_split(const kvr_ctx *c, int tiles, int K, int R, int fw) {
+    const char *env = getenv("KVR_SKINNY_SPLIT");
+    const int ksteps = K / 32;
+    const int smax = std::max(1, ksteps / 32);
+    int s = env ? atoi(env) : std::max(1, (1024 + tiles - 1) / tiles);
+    s = std::max(1, std::min(s, smax));
+    while (s > 1 && (size_t)tiles * s * R * fw > c->skinny_part_floats) --s;
+    return s;
+}
+
+hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
+    if (!c->bf16 || c->force_simple) return launch_linear_simple(c->bf16, epi, a, s);
+    const int ncols = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+    const bool kok = a.K % 32 == 0 && a.ldx % 8 == 0;
+    if (a.R <= 64 && kok) {
+        const int nt = (ncols % 64 == 0) ? 4 : (ncols % 32 == 0 ? 2 : 0);
+        if (nt) {
+            const int fw = 16 * nt;
+            const int tiles = ncols / fw;
+            if (tiles <= c->n_counters)
+                return launch_linear_skinny(epi, a, skinny_split(c, tiles, a.K, a.R, fw), nt, s);
+        }
+    }
+    if (a.K % 64 == 0 && a.ldx % 8 == 0 && (epi == EPI_SWIGLU ? a.N % 64 == 0 : a.N % 128 == 0))
+        return launch_linear_tiled(epi, a, s);
+    return launch_linear_simple(c->bf16, epi, a, s);
+}
+
+LinearArgs make_args(const void *x, int ldx, int R, int K, int N, const void *w0, const void *w1, const void *w2,
+                     int e0, int e1, void *out, int ldo, kvr_ctx *c) {
+    LinearArgs a{};
+    a.x = x; a.ldx = ldx; a.R = R; a.K = K; a.N = N;
+    a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
+    a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
+    a.out = out; a.ldo = ldo;
+    a.partial = c->skinny_part; a.counters = c->counters;
+    return a;
+}
+
+// Upload the tables of a pass and enqueue its kernels.
+kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
+    const kvr_dims &d = c->d;
+    const int R = (int)t.rows.size();
+    if (R == 0) return KVR_OK;
+    const bool attn_mfma = c->bf16 && !c->force_simple && d.head_dim == ATT_HD && d.n_heads / d.n_kv_heads <= 8;
+    if (attn_mfma) plan_attention(c, t);
+    if ((int)t.items.size() > c->items_cap || (int)t.comb.size() > c->comb_cap)
+        return fail(c, KVR_E_RANGE, "attention plan exceeds the context's item capacity");
+
+    // pack the tables: rows | docs | items | combine
+    const size_t o_docs = align_up(t.rows.size() * sizeof(RowInfo), 256);
+    const size_t o_items = o_docs + align_up(t.docs.size() * sizeof(DocInfo), 256);
+    const size_t o_comb = o_items + align_up(t.items.size() * sizeof(AttnItem), 256);
+    const size_t total = o_comb + t.comb.size() * sizeof(CombineItem);
+    if (total > c->tables_bytes) return fail(c, KVR_E_RANGE, "pass tables exceed the context's staging capacity");
+    if (c->stage_pending) {
+        hipError_t e = hipEventSynchronize(c->stage_ev);
+        if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize(staging)");
+        c->stage_pending = false;
+    }
+    memcpy(c->h_stage, t.rows.data(), t.rows.size() * sizeof(RowInfo));
+    memcpy(c->h_stage + o_docs, t.docs.data(), t.docs.size() * sizeof(DocInfo));
+    if (!t.items.empty()) memcpy(c->h_stage + o_items, t.items.data(), t.items.size() * sizeof(AttnItem));
+    if (!t.comb.empty()) memcpy(c->h_stage + o_comb, t.comb.data(), t.comb.size() * sizeof(CombineItem));
+    hipError_t e = hipMemcpyAsync(c->d_tables, c->h_stage, total, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync(tables)");
+    e = hipEventRecord(c->stage_ev, s);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord(staging)");
+    c->stage_pending = true;
+    const RowInfo *rows = (const RowInfo *)c->d_tables;
+    const DocInfo *docs = (const DocInfo *)(c->d_tables + o_docs);
+    const AttnItem *items = (const AttnItem *)(c->d_tables + o_items);
+    const CombineItem *comb = (const CombineItem *)(c->d_tables + o_comb);
+
+    const int D = d.d_model, F = d.d_ffn, hd = d.head_dim;
+    const int qd = d.n_heads * hd, kd = d.n_kv_heads * hd;
+    const bool bf = c->bf16;
+#define KVR_CHECK(expr, what)                          \
+    do {                                               \
+        hipError_t err_ = (expr);                      \
+        if (err_ != hipSuccess) return hip_fail(c, err_, what); \
+    } while (0)
+
+    KVR_CHECK(launch_embed(bf, rows, docs, R, c->embed, D, d.vocab, c->H, s), "embed");
+    for (int l = 0; l < d.n_layers; ++l) {
+        const kvr_layer_weights &w = c->layers[l];
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, w.attn_norm, R, D, d.rms_eps, c->Xn, D, s), "rmsnorm(attn)");
+        KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, D, R, D, qd + 2 * kd, w.wq, w.wk, w.wv, qd, qd + kd, c->QKV,
+                                                 qd + 2 * kd, c), s), "linear(qkv)");
+        KVR_CHECK(launch_rope_scatter(bf, c->QKV, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd,
+                                      c->rope_cos, c->rope_sin, c->Qb, s), "rope_scatter");
+        if (attn_mfma) {
+            KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, rows, docs, items, (int)t.items.size(), l,
+                                            d.n_heads, d.n_kv_heads, c->attn_part, (bf16_t *)c->Ob, s), "attention");
+            KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
+                                               (bf16_t *)c->Ob, s), "attention_combine");
+        } else {
+            KVR_CHECK(launch_attention_simple(bf, c->Qb, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob, s),
+                      "attention_simple");
+        }
+        KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, D, c), s),
+                  "linear(o)");
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, w.mlp_norm, R, D, d.rms_eps, c->Xn, D, s), "rmsnorm(mlp)");
+        KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, F, c), s),
+                  "linear(gate_up)");
+        KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H, D, c), s),
+                  "linear(down)");
+    }
+    KVR_CHECK(launch_final_norm(bf, c->H, c->final_norm, rows, docs, R, D, d.rms_eps, s), "final_norm");
+#undef KVR_CHECK
+    return KVR_OK;
+}
+
+kvr_status check_dims(const kvr_dims *d) {
+    if (!d) return KVR_E_ARG;
+    if (d->n_layers < 1 || d->d_model < 1 || d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 2 ||
+        d->d_ffn < 1 || d->vocab < 1 || d->max_ctx < 1 || d->max_rows < 1)
+        return KVR_E_ARG;
+    if (d->n_heads % d->n_kv_heads != 0 || d->head_dim % 2 != 0) return KVR_E_ARG;
+    if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.0)) return KVR_E_ARG;
+    if (d->dtype != KVR_F32 && d->dtype != KVR_BF16) return KVR_E_ARG;
+    if (d->head_dim > 128) return KVR_E_UNSUPPORTED;
+    return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kvr_cache_bytes(const kvr_dims *d, int32_t n_cap) {
+    if (!d || n_cap < 0 || check_dims(d) != KVR_OK) return 0;
+    return (size_t)d->n_layers * 2 * d->n_kv_heads * (size_t)n_cap * d->head_dim * elem_size(*d);
+}
+
+size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes : 0; }
+
+const char *kvr_last_error(const kvr_ctx *c) { return c ? c->err.c_str() : g_error.c_str(); }
+
+kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **out) {
+    if (!out) return fail(nullptr, KVR_E_ARG, "kvr_create: out is NULL");
+    *out = nullptr;
+    kvr_status st = check_dims(dims);
+    if (st != KVR_OK)
+        return fail(nullptr, st, st == KVR_E_UNSUPPORTED ? "kvr_create: head_dim > 128 is not supported"
+                                                         : "kvr_create: invalid dims");
+    if (!wts || !wts->embed || !wts->final_norm || !wts->layers)
+        return fail(nullptr, KVR_E_ARG, "kvr_create: NULL weights");
+    const kvr_dims &d = *dims;
+    if (!aligned16(wts->embed) || !aligned16(wts->final_norm))
+        return fail(nullptr, KVR_E_ARG, "kvr_create: weights must be 16-byte aligned");
+    for (int l = 0; l < d.n_layers; ++l) {
+        const kvr_layer_weights &w = wts->layers[l];
+        const void *req[] = {w.attn_norm, w.wq, w.wk, w.wv, w.wo, w.mlp_norm, w.w_gate, w.w_up, w.w_down};
+        for (const void *p : req)
+            if (!p || !aligned16(p)) return fail(nullptr, KVR_E_ARG, "kvr_create: missing or misaligned layer weight");
+        const void *bias[] = {w.bq, w.bk, w.bv};
+        for (const void *p : bias) {
+            if (d.qkv_bias && (!p || !aligned16(p)))
+                return fail(nullptr, KVR_E_ARG, "kvr_create: qkv_bias set but a bias is missing or misaligned");
+            if (!d.qkv_bias && p) return fail(nullptr, KVR_E_ARG, "kvr_create: bias given but qkv_bias is 0");
+        }
+    }
+
+    kvr_ctx *c = new kvr_ctx();
+    c->d = d;
+    c->bf16 = d.dtype == KVR_BF16;
+    const char *fs = getenv("KVR_SIMPLE");
+    c->force_simple = fs && fs[0] == '1';
+    c->layers.assign(wts->layers, wts->layers + d.n_layers);
+    c->embed = wts->embed;
+    c->final_norm = wts->final_norm;
+    hipError_t e = hipGetDevice(&c->device);
+    if (e != hipSuccess) { delete c; return hip_fail(nullptr, e, "hipGetDevice"); }
+
+    const int D = d.d_model, F = d.d_ffn, hd = d.head_dim;
+    const int qd = d.n_heads * hd, kd = d.n_kv_heads * hd;
+    const size_t es = elem_size(d);
+    c->rows_cap = std::max(d.max_rows, std::min(d.max_ctx, PREFILL_CHUNK));
+    c->max_docs = std::max(1, d.max_rows);
+    const int G = d.n_heads / d.n_kv_heads;
+    c->attn_part_floats = ATTN_PART_BYTES / 4;
+    const size_t slot_floats = (size_t)G * ATT_ROWS * PART_ROW;
+    const int max_slots = (int)(c->attn_part_floats / slot_floats);
+    const int blocks_cap = c->rows_cap / ATT_ROWS + c->max_docs + 1;
+    c->items_cap = blocks_cap * d.n_kv_heads + max_slots;
+    c->comb_cap = blocks_cap * d.n_kv_heads;
+    c->skinny_part_floats = SKINNY_PART_BYTES / 4;
+    c->n_counters = N_COUNTERS;
+    c->tables_bytes = align_up((size_t)c->rows_cap * sizeof(RowInfo), 256) +
+                      align_up((size_t)c->max_docs * sizeof(DocInfo), 256) +
+                      align_up((size_t)c->items_cap * sizeof(AttnItem), 256) + (size_t)c->comb_cap * sizeof(CombineItem);
+
+    const size_t R = (size_t)c->rows_cap;
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+    const size_t o_H = take(R * D * 4), o_QKV = take(R * (qd + 2 * kd) * 4), o_Xn = take(R * D * es),
+                 o_Qb = take(R * qd * es), o_Ob = take(R * qd * es), o_Ab = take(R * F * es),
+                 o_cos = take((size_t)d.max_ctx * (hd / 2) * 4), o_sin = take((size_t)d.max_ctx * (hd / 2) * 4),
+                 o_sp = take(c->skinny_part_floats * 4), o_cnt = take((size_t)c->n_counters * 4),
+                 o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes);
+    c->ws_bytes = off;
+    e = hipMalloc((void **)&c->ws, c->ws_bytes);
+    if (e != hipSuccess) { delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: workspace allocation failed"); }
+    c->H = (float *)(c->ws + o_H);
+    c->QKV = (float *)(c->ws + o_QKV);
+    c->Xn = c->ws + o_Xn;
+    c->Qb = c->ws + o_Qb;
+    c->Ob = c->ws + o_Ob;
+    c->Ab = c->ws + o_Ab;
+    c->rope_cos = (float *)(c->ws + o_cos);
+    c->rope_sin = (float *)(c->ws + o_sin);
+    c->skinny_part = (float *)(c->ws + o_sp);
+    c->counters = (int *)(c->ws + o_cnt);
+    c->attn_part = (float *)(c->ws + o_ap);
+    c->d_tables = c->ws + o_tab;
+
+    e = hipHostMalloc((void **)&c->h_stage, c->tables_bytes, hipHostMallocDefault);
+    if (e != hipSuccess) { (void)hipFree(c->ws); delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: pinned staging allocation failed"); }
+    e = hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
+    if (e != hipSuccess) { (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c; return hip_fail(nullptr, e, "hipEventCreate"); }
+
+    // rotary table: angles p * theta^(-2i/hd) in double precision, stored as fp32 cos/sin
+    {
+        const int half = hd / 2;
+        std::vector<float> tc((size_t)d.max_ctx * half), ts((size_t)d.max_ctx * half);
+        std::vector<double> inv(half);
+        for (int i = 0; i < half; ++i) inv[i] = std::pow(d.rope_theta, -2.0 * i / (double)hd);
+        for (int p = 0; p < d.max_ctx; ++p)
+            for (int i = 0; i < half; ++i) {
+                const double a = (double)p * inv[i];
+                tc[(size_t)p * half + i] = (float)std::cos(a);
+                ts[(size_t)p * half + i] = (float)std::sin(a);
+            }
+        e = hipMemcpy(c->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(c->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemset(c->counters, 0, (size_t)c->n_counters * 4);
+        if (e != hipSuccess) {
+            (void)hipEventDestroy(c->stage_ev); (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c;
+            return hip_fail(nullptr, e, "kvr_create: workspace initialisation");
+        }
+    }
+    *out = c;
+    return KVR_OK;
+}
+
+void kvr_destroy(kvr_ctx *c) {
+    if (!c) return;
+    {
+        DeviceGuard g(c->device);
+        (void)hipDeviceSynchronize();
+        if (c->stage_ev) (void)hipEventDestroy(c->stage_ev);
+        if (c->h_stage) (void)hipHostFree(c->h_stage);
+        if (c->ws) (void)hipFree(c->ws);
+    }
+    delete c;
+}
+
+kvr_status kvr_prefill(kvr_ctx *c, const int32_t *d_tokens, int32_t n, int32_t n_cap, void *d_cache,
+                       float *d_hidden_out, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_prefill: NULL context");
+    if (!d_tokens || !d_cache) return fail(c, KVR_E_ARG, "kvr_prefill: NULL tokens or cache");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_prefill: cache must be 16-byte aligned");
+    if (n < 1 || n > n_cap || n_cap > c->d.max_ctx)
+        return fail(c, KVR_E_RANGE, "kvr_prefill: need 1 <= n <= n_cap <= max_ctx");
+    DeviceGuard g(c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const int chunk = c->rows_cap;
+    for (int c0 = 0; c0 < n; c0 += chunk) {
+        const int c1 = std::min(n, c0 + chunk);
+        Tables t;
+        t.docs.push_back(DocInfo{d_cache, d_tokens, d_hidden_out, n, n_cap, 0, c1 - c0});
+        t.rows.reserve(c1 - c0);
+        for (int p = c0; p < c1; ++p) t.rows.push_back(RowInfo{p, 0, p, 0});
+        kvr_status st = run_pass(c, t, s);
+        if (st != KVR_OK) return st;
+    }
+    return KVR_OK;
+}
+
+kvr_status kvr_linear(kvr_ctx *c, kvr_epilogue epi, const void *d_x, int32_t rows, int32_t in_features,
+                      const void *d_w, const void *d_w2, int32_t out_features, void *d_out, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_linear: NULL context");
+    if (epi != KVR_EPI_STORE && epi != KVR_EPI_ADD && epi != KVR_EPI_SWIGLU)
+        return fail(c, KVR_E_ARG, "kvr_linear: unknown epilogue");
+    if (!d_x || !d_w || !d_out || (epi == KVR_EPI_SWIGLU) != (d_w2 != nullptr))
+        return fail(c, KVR_E_ARG, "kvr_linear: NULL pointer (d_w2 is required for SWIGLU only)");
+    if (!aligned16(d_x) || !aligned16(d_w) || !aligned16(d_out) || (d_w2 && !aligned16(d_w2)))
+        return fail(c, KVR_E_ARG, "kvr_linear: pointers must be 16-byte aligned");
+    if (rows < 1 || rows > c->rows_cap || in_features < 1 || out_features < 1)
+        return fail(c, KVR_E_RANGE, "kvr_linear: rows must be in [1, row capacity] and features positive");
+    DeviceGuard g(c->device);
+    const int e = epi == KVR_EPI_STORE ? EPI_STORE : (epi == KVR_EPI_ADD ? EPI_RESID : EPI_SWIGLU);
+    const void *w1 = d_w2 ? d_w2 : d_w;
+    LinearArgs a = make_args(d_x, in_features, rows, in_features, out_features, d_w, w1, w1, out_features,
+                             out_features, d_out, out_features, c);
+    hipError_t err = linear(c, e, a, (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(c, err, "kvr_linear");
+    return KVR_OK;
+}
+
+kvr_status kvr_repair(kvr_ctx *c, const kvr_doc *docs, int32_t n_docs, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_repair: NULL context");
+    if (n_docs < 0 || (n_docs > 0 && !docs)) return fail(c, KVR_E_ARG, "kvr_repair: bad document array");
+    long long total = 0;
+    for (int i = 0; i < n_docs; ++i) {
+        const kvr_doc &dc = docs[i];
+        const std::string tag = "kvr_repair: document " + std::to_string(i) + ": ";
+        if (dc.n_positions < 0 || (dc.n_positions > 0 && !dc.h_positions))
+            return fail(c, KVR_E_ARG, tag + "bad position list");
+        if (dc.n < 1 || dc.n > dc.n_cap || dc.n_cap > c->d.max_ctx)
+            return fail(c, KVR_E_RANGE, tag + "need 1 <= n <= n_cap <= max_ctx");
+        if (dc.edit_start < 0 || dc.edit_start > dc.edit_end || dc.edit_end > dc.n)
+            return fail(c, KVR_E_RANGE, tag + "need 0 <= edit_start <= edit_end <= n");
+        for (int j = 0; j < dc.n_positions; ++j) {
+            const int p = dc.h_positions[j];
+            if (p < 0 || p >= dc.n) return fail(c, KVR_E_RANGE, tag + "position outside [0, n)");
+            if (j > 0 && p <= dc.h_positions[j - 1])
+                return fail(c, KVR_E_ARG, tag + "positions must be strictly ascending");
+            if (p >= dc.edit_start && p < dc.edit_end) return fail(c, KVR_E_ARG, tag + "position inside the edit span");
+        }
+        const long long np = (long long)(dc.edit_end - dc.edit_start) + dc.n_positions;
+        if (np > 0 && (!dc.d_cache || !dc.d_tokens_new)) return fail(c, KVR_E_ARG, tag + "NULL cache or tokens");
+        if (np > 0 && !aligned16(dc.d_cache)) return fail(c, KVR_E_ARG, tag + "cache must be 16-byte aligned");
+        total += np;
+    }
+    if (total > c->d.max_rows) return fail(c, KVR_E_RANGE, "kvr_repair: total |P| exceeds max_rows");
+    if (total == 0) return KVR_OK;
+
+    Tables t;
+    t.rows.reserve((size_t)total);
+    for (int i = 0; i < n_docs; ++i) {
+        const kvr_doc &dc = docs[i];
+        const int np = (dc.edit_end - dc.edit_start) + dc.n_positions;
+        if (np == 0) continue;
+        const int di = (int)t.docs.size();
+        t.docs.push_back(DocInfo{dc.d_cache, dc.d_tokens_new, dc.d_hidden_out, dc.n, dc.n_cap, (int)t.rows.size(), np});
+        // merge the span and the (sorted, disjoint) positions in ascending order
+        int j = 0, out = 0;
+        for (int p = dc.edit_start; p <= dc.edit_end; ++p) {
+            while (j < dc.n_positions && dc.h_positions[j] < p) t.rows.push_back(RowInfo{dc.h_positions[j++], di, out++, 0});
+            if (p < dc.edit_end) t.rows.push_back(RowInfo{p, di, out++, 0});
+        }
+        while (j < dc.n_positions) t.rows.push_back(RowInfo{dc.h_positions[j++], di, out++, 0});
+    }
+    DeviceGuard g(c->device);
+    return run_pass(c, t, (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,145 @@
+// Tiled bf16 MFMA linear layer for many rows (prefill, batched repair).
+//
+// Y[r][n] = sum_k X[r][k] * W[n][k]: both operands are K-contiguous, so a
+// 128x128 output tile streams 64-wide K slabs of X and W through LDS (rows
+// padded to 144 B so that the 16-byte operand reads of a wavefront spread over
+// the banks), and each of the four wavefronts computes a 64x64 sub-tile as
+// 4x4 v_mfma_f32_16x16x32_bf16 tiles.  The next slab is fetched into
+// registers while the current one is multiplied.
+#include "common.h"
+
+namespace kvr {
+
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row (144 B)
+
+__device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
+
+template <int EPI>
+__global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
+    __shared__ __attribute__((aligned(16))) bf16_t As[BM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[BN * LDS_STRIDE];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int wm = w >> 1, wn = w & 1;
+    const int bn = blockIdx.x, bm = blockIdx.y;
+    const int K = a.K;
+
+    // global -> register loader: thread covers rows tid/8 + 32*i, 16 bytes at k (tid%8)*8
+    const int lrow = tid >> 3, lk = (tid & 7) * 8;
+    const bf16_t *ag[4];
+    const bf16_t *bg[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = min(bm * BM + lrow + 32 * i, a.R - 1);
+        ag[i] = (const bf16_t *)a.x + (size_t)r * a.ldx + lk;
+        const int c = lrow + 32 * i;  // B-tile row (output column of the tile)
+        const bf16_t *base;
+        int row;
+        if (EPI == EPI_SWIGLU) {
+            const int half = c >> 6, j = c & 63;
+            base = (const bf16_t *)a.w[j < 32 ? 0 : 1];
+            row = bn * 64 + half * 32 + (j & 31);
+        } else {
+            const int n = bn * BN + c;
+            if (n < a.seg_end[0]) { base = (const bf16_t *)a.w[0]; row = n; }
+            else if (n < a.seg_end[1]) { base = (const bf16_t *)a.w[1]; row = n - a.seg_end[0]; }
+            else { base = (const bf16_t *)a.w[2]; row = n - a.seg_end[1]; }
+        }
+        bg[i] = base + (size_t)row * K + lk;
+    }
+
+    uint4 ra[4], rb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        ra[i] = *reinterpret_cast<const uint4 *>(ag[i]);
+        rb[i] = *reinterpret_cast<const uint4 *>(bg[i]);
+    }
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int koff = 8 * (lane >> 4);
+    for (int k0 = 0; k0 < K; k0 += BK) {
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            *reinterpret_cast<uint4 *>(&As[(lrow + 32 * i) * LDS_STRIDE + lk]) = ra[i];
+            *reinterpret_cast<uint4 *>(&Bs[(lrow + 32 * i) * LDS_STRIDE + lk]) = rb[i];
+        }
+        __syncthreads();
+        if (k0 + BK < K) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ra[i] = *reinterpret_cast<const uint4 *>(ag[i] + k0 + BK);
+                rb[i] = *reinterpret_cast<const uint4 *>(bg[i] + k0 + BK);
+            }
+        }
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+            bf16x8 av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                av[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * 64 + i * 16 + (lane & 15)) * LDS_STRIDE + ks * 32 + koff]);
+                bv[i] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * 64 + i * 16 + (lane & 15)) * LDS_STRIDE + ks * 32 + koff]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+        }
+    }
+
+    // accumulator layout: lane l holds tile column l%16, rows 4*(l/16)+e
+    const int rbase = bm * BM + wm * 64 + 4 * (lane >> 4);
+    if (EPI == EPI_SWIGLU) {
+        bf16_t *A = (bf16_t *)a.out;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = rbase + i * 16 + e;
+                if (r >= a.R) continue;
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int f = bn * 64 + wn * 32 + j * 16 + (lane & 15);
+                    A[(size_t)r * a.ldo + f] = f32_to_bf16(silu_f(acc[i][j][e]) * acc[i][j + 2][e]);
+                }
+            }
+        return;
+    }
+    float *out = (float *)a.out;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = rbase + i * 16 + e;
+            if (r >= a.R) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float *o = out + (size_t)r * a.ldo + bn * BN + wn * 64 + j * 16 + (lane & 15);
+                if (EPI == EPI_RESID) *o += acc[i][j][e];
+                else *o = acc[i][j][e];
+            }
+        }
+}
+
+}  // namespace
+
+hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
+    if (a.R <= 0) return hipSuccess;
+    const int nb = epi == EPI_SWIGLU ? a.N / 64 : a.N / BN;
+    dim3 grid(nb, (a.R + BM - 1) / BM);
+    if (epi == EPI_STORE) hipLaunchKernelGGL(linear_tiled_kernel<EPI_STORE>, grid, dim3(256), 0, s, a);
+    else if (epi == EPI_RESID) hipLaunchKernelGGL(linear_tiled_kernel<EPI_RESID>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(linear_tiled_kernel<EPI_SWIGLU>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace kvr

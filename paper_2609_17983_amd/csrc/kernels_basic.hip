@@ -1,0 +1,328 @@
+// Row-wise kernels of the decoder pass (embedding gather, RMSNorm, rotary
+// embedding + cache scatter) and the straightforward attention / linear kernels
+// used for fp32 models and for shapes the MFMA kernels do not cover.
+#include <math.h>
+
+#include "common.h"
+
+namespace kvr {
+
+namespace {
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Sum over a 256-thread block.
+__device__ __forceinline__ float block_sum256(float v, float *red) {
+    v = warp_sum(v);
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    if (l == 0) red[w] = v;
+    __syncthreads();
+    float t = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    return t;
+}
+
+// Token ids outside [0, vocab) are clamped into range rather than read out of bounds.
+template <typename TW>
+__global__ __launch_bounds__(256) void embed_kernel(const RowInfo *rows, const DocInfo *docs, const TW *embed,
+                                                    int d, int vocab, float *H) {
+    const int r = blockIdx.x;
+    const RowInfo ri = rows[r];
+    const int tok = min(max(docs[ri.doc].tokens[ri.pos], 0), vocab - 1);
+    const TW *src = embed + (size_t)tok * d;
+    for (int i = threadIdx.x; i < d; i += 256) H[(size_t)r * d + i] = to_f32(src[i]);
+}
+
+// X = H * rsqrt(mean(H^2) + eps) * gain, written in the operand type.
+template <typename TO, typename TG>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float *H, const TG *gain, int d, float eps, TO *X,
+                                                      int ldx) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    const float *h = H + (size_t)r * d;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) ss += h[i] * h[i];
+    ss = block_sum256(ss, red);
+    const float inv = rsqrtf(ss / (float)d + eps);
+    for (int i = threadIdx.x; i < d; i += 256) X[(size_t)r * ldx + i] = from_f32<TO>(h[i] * inv * to_f32(gain[i]));
+}
+
+template <typename TG>
+__global__ __launch_bounds__(256) void final_norm_kernel(const float *H, const TG *gain, const RowInfo *rows,
+                                                         const DocInfo *docs, int d, float eps) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    const RowInfo ri = rows[r];
+    float *dst = docs[ri.doc].hidden_out;
+    if (!dst) return;
+    dst += (size_t)ri.out * d;
+    const float *h = H + (size_t)r * d;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) ss += h[i] * h[i];
+    ss = block_sum256(ss, red);
+    const float inv = rsqrtf(ss / (float)d + eps);
+    for (int i = threadIdx.x; i < d; i += 256) dst[i] = h[i] * inv * to_f32(gain[i]);
+}
+
+// Adds the Q/K/V bias, rotates Q and K at the row's absolute position
+// (rotate-half pairing) and scatters K and V into the row's cache slot; Q goes
+// to the attention operand buffer [R][Hq*hd].
+template <typename T>
+__global__ __launch_bounds__(256) void rope_scatter_kernel(const float *qkv, const T *bq, const T *bk, const T *bv,
+                                                           const RowInfo *rows, const DocInfo *docs, int layer,
+                                                           int Hq, int Hkv, int hd, const float *rcos,
+                                                           const float *rsin, T *Q) {
+    const int r = blockIdx.x;
+    const RowInfo ri = rows[r];
+    const DocInfo dc = docs[ri.doc];
+    const int half = hd >> 1;
+    const int qd = Hq * hd, kd = Hkv * hd;
+    const float *row = qkv + (size_t)r * (qd + 2 * kd);
+    const float *cs = rcos + (size_t)ri.pos * half;
+    const float *sn = rsin + (size_t)ri.pos * half;
+    T *cache = (T *)dc.cache;
+    const size_t head_stride = (size_t)dc.n_cap * hd;
+    T *kbase = cache + ((size_t)layer * 2 + 0) * Hkv * head_stride + (size_t)ri.pos * hd;
+    T *vbase = cache + ((size_t)layer * 2 + 1) * Hkv * head_stride + (size_t)ri.pos * hd;
+    for (int idx = threadIdx.x; idx < (Hq + Hkv) * half; idx += 256) {
+        const int j = idx / half, i = idx - j * half;
+        float a, b;
+        if (j < Hq) {
+            a = row[j * hd + i];
+            b = row[j * hd + i + half];
+            if (bq) { a += to_f32(bq[j * hd + i]); b += to_f32(bq[j * hd + i + half]); }
+        } else {
+            const int g = j - Hq;
+            a = row[qd + g * hd + i];
+            b = row[qd + g * hd + i + half];
+            if (bk) { a += to_f32(bk[g * hd + i]); b += to_f32(bk[g * hd + i + half]); }
+        }
+        const float c = cs[i], s = sn[i];
+        const float o1 = a * c - b * s, o2 = b * c + a * s;
+        if (j < Hq) {
+            Q[(size_t)r * qd + j * hd + i] = from_f32<T>(o1);
+            Q[(size_t)r * qd + j * hd + i + half] = from_f32<T>(o2);
+        } else {
+            const int g = j - Hq;
+            kbase[g * head_stride + i] = from_f32<T>(o1);
+            kbase[g * head_stride + i + half] = from_f32<T>(o2);
+        }
+    }
+    for (int idx = threadIdx.x; idx < kd; idx += 256) {
+        const int g = idx / hd, i = idx - g * hd;
+        float v = row[qd + kd + idx];
+        if (bv) v += to_f32(bv[idx]);
+        vbase[g * head_stride + i] = from_f32<T>(v);
+    }
+}
+
+// One wavefront per (row, query head): online softmax over keys 0..pos.
+template <typename T>
+__global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const RowInfo *rows, const DocInfo *docs,
+                                                              int layer, int Hq, int Hkv, int hd, T *O) {
+    const int r = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
+    const RowInfo ri = rows[r];
+    const DocInfo dc = docs[ri.doc];
+    const int g = j / (Hq / Hkv);
+    const size_t head_stride = (size_t)dc.n_cap * hd;
+    const T *K = (const T *)dc.cache + (((size_t)layer * 2 + 0) * Hkv + g) * head_stride;
+    const T *V = (const T *)dc.cache + (((size_t)layer * 2 + 1) * Hkv + g) * head_stride;
+    const int qd = Hq * hd;
+    const bool has0 = lane < hd, has1 = lane + 64 < hd;
+    const float scale = 1.0f / sqrtf((float)hd);
+    const float q0 = has0 ? to_f32(Q[(size_t)r * qd + j * hd + lane]) * scale : 0.f;
+    const float q1 = has1 ? to_f32(Q[(size_t)r * qd + j * hd + lane + 64]) * scale : 0.f;
+    float m = -INFINITY, l = 0.f, a0 = 0.f, a1 = 0.f;
+    for (int t = 0; t <= ri.pos; ++t) {
+        const T *kr = K + (size_t)t * hd;
+        float p = (has0 ? q0 * to_f32(kr[lane]) : 0.f) + (has1 ? q1 * to_f32(kr[lane + 64]) : 0.f);
+        p = warp_sum(p);
+        const float mn = fmaxf(m, p);
+        const float corr = expf(m - mn);
+        const float e = expf(p - mn);
+        const T *vr = V + (size_t)t * hd;
+        l = l * corr + e;
+        a0 = a0 * corr + (has0 ? e * to_f32(vr[lane]) : 0.f);
+        a1 = a1 * corr + (has1 ? e * to_f32(vr[lane + 64]) : 0.f);
+        m = mn;
+    }
+    const float inv = 1.0f / l;
+    if (has0) O[(size_t)r * qd + j * hd + lane] = from_f32<T>(a0 * inv);
+    if (has1) O[(size_t)r * qd + j * hd + lane + 64] = from_f32<T>(a1 * inv);
+}
+
+__device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
+
+// Generic tiled linear layer: 64x64 output tile, 16-wide K steps, 4x4 outputs
+// per thread.  Every index is bounds-checked, so any R, N, K works.
+template <typename T, int EPI>
+__global__ __launch_bounds__(256) void linear_simple_kernel(LinearArgs a) {
+    __shared__ float xs[16][65];
+    __shared__ float ws[16][65];
+    __shared__ float tile[64][65];
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    const int r0 = blockIdx.y * 64;
+    const int c0 = blockIdx.x * 64;
+    const T *X = (const T *)a.x;
+    // weight row pointer of the tile's column c (0..63); null if out of range
+    auto wrow = [&](int c) -> const T * {
+        if (EPI == EPI_SWIGLU) {
+            const int f = blockIdx.x * 32 + (c & 31);
+            if (f >= a.N) return nullptr;
+            return (const T *)a.w[c >> 5] + (size_t)f * a.K;
+        }
+        const int n = c0 + c;
+        if (n >= a.N) return nullptr;
+        if (n < a.seg_end[0]) return (const T *)a.w[0] + (size_t)n * a.K;
+        if (n < a.seg_end[1]) return (const T *)a.w[1] + (size_t)(n - a.seg_end[0]) * a.K;
+        return (const T *)a.w[2] + (size_t)(n - a.seg_end[1]) * a.K;
+    };
+    float acc[4][4] = {};
+    const int lr = threadIdx.x >> 2;        // 0..63: tile row / column loaded
+    const int lk = (threadIdx.x & 3) * 4;   // 0,4,8,12
+    const T *wr = wrow(lr);
+    const int xr = r0 + lr;
+    for (int k0 = 0; k0 < a.K; k0 += 16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int k = k0 + lk + e;
+            xs[lk + e][lr] = (xr < a.R && k < a.K) ? to_f32(X[(size_t)xr * a.ldx + k]) : 0.f;
+            ws[lk + e][lr] = (wr && k < a.K) ? to_f32(wr[k]) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            float xv[4], wv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) { xv[i] = xs[kk][ty * 4 + i]; wv[i] = ws[kk][tx * 4 + i]; }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) acc[i][jj] += xv[i] * wv[jj];
+        }
+        __syncthreads();
+    }
+    if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) tile[ty * 4 + i][tx * 4 + jj] = acc[i][jj];
+        __syncthreads();
+        T *A = (T *)a.out;
+        for (int idx = threadIdx.x; idx < 64 * 32; idx += 256) {
+            const int rr = idx >> 5, f = idx & 31;
+            const int row = r0 + rr, feat = blockIdx.x * 32 + f;
+            if (row < a.R && feat < a.N)
+                A[(size_t)row * a.ldo + feat] = from_f32<T>(silu_f(tile[rr][f]) * tile[rr][32 + f]);
+        }
+        return;
+    }
+    float *out = (float *)a.out;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = r0 + ty * 4 + i;
+        if (row >= a.R) continue;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int n = c0 + tx * 4 + jj;
+            if (n >= a.N) continue;
+            if (EPI == EPI_RESID) out[(size_t)row * a.ldo + n] += acc[i][jj];
+            else out[(size_t)row * a.ldo + n] = acc[i][jj];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int R, const void *embed, int d,
+                        int vocab, float *H, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(R), dim3(256), 0, s, rows, docs, (const bf16_t *)embed, d, vocab,
+                           H);
+    else
+        hipLaunchKernelGGL(embed_kernel<float>, dim3(R), dim3(256), 0, s, rows, docs, (const float *)embed, d, vocab,
+                           H);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, const float *H, const void *gain, int R, int d, float eps,
+                          void *X, int ldx, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (bf16_out && bf16_gain)
+        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, d, eps,
+                           (bf16_t *)X, ldx);
+    else if (!bf16_out && !bf16_gain)
+        hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(R), dim3(256), 0, s, H, (const float *)gain, d, eps,
+                           (float *)X, ldx);
+    else if (bf16_out)
+        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, float>), dim3(R), dim3(256), 0, s, H, (const float *)gain, d, eps,
+                           (bf16_t *)X, ldx);
+    else
+        hipLaunchKernelGGL((rmsnorm_kernel<float, bf16_t>), dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, d, eps,
+                           (float *)X, ldx);
+    return hipGetLastError();
+}
+
+hipError_t launch_final_norm(bool bf16_gain, const float *H, const void *gain, const RowInfo *rows,
+                             const DocInfo *docs, int R, int d, float eps, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (bf16_gain)
+        hipLaunchKernelGGL(final_norm_kernel<bf16_t>, dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, rows, docs,
+                           d, eps);
+    else
+        hipLaunchKernelGGL(final_norm_kernel<float>, dim3(R), dim3(256), 0, s, H, (const float *)gain, rows, docs, d,
+                           eps);
+    return hipGetLastError();
+}
+
+hipError_t launch_rope_scatter(bool bf16, const float *qkv, const void *bq, const void *bk, const void *bv,
+                               const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd,
+                               const float *rope_cos, const float *rope_sin, void *Q, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, dim3(R), dim3(256), 0, s, qkv, (const bf16_t *)bq,
+                           (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
+                           (bf16_t *)Q);
+    else
+        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(256), 0, s, qkv, (const float *)bq,
+                           (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
+                           (float *)Q);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
+                                   int layer, int Hq, int Hkv, int hd, void *O, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q, rows, docs,
+                           layer, Hq, Hkv, hd, (bf16_t *)O);
+    else
+        hipLaunchKernelGGL(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q, rows, docs,
+                           layer, Hq, Hkv, hd, (float *)O);
+    return hipGetLastError();
+}
+
+hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s) {
+    if (a.R <= 0) return hipSuccess;
+    const int cols_per_block = epi == EPI_SWIGLU ? 32 : 64;
+    dim3 grid((a.N + cols_per_block - 1) / cols_per_block, (a.R + 63) / 64);
+#define KVR_LS(T, E) hipLaunchKernelGGL((linear_simple_kernel<T, E>), grid, dim3(256), 0, s, a)
+    if (bf16) {
+        if (epi == EPI_STORE) KVR_LS(bf16_t, EPI_STORE);
+        else if (epi == EPI_RESID) KVR_LS(bf16_t, EPI_RESID);
+        else KVR_LS(bf16_t, EPI_SWIGLU);
+    } else {
+        if (epi == EPI_STORE) KVR_LS(float, EPI_STORE);
+        else if (epi == EPI_RESID) KVR_LS(float, EPI_RESID);
+        else KVR_LS(float, EPI_SWIGLU);
+    }
+#undef KVR_LS
+    return hipGetLastError();
+}
+
+}  // namespace kvr

@@ -1,0 +1,266 @@
+"""GPU parity of kvr_prefill / kvr_repair against the fp64 oracle, at sizes the
+oracle finishes in seconds (several tiles, ragged tails).
+
+* The tiny fp32 Llama-style decoder of the workload list (2 layers, d_model 256,
+  4 heads x 64, FFN 688, vocab 1024, 512-token context, 8-token edit at 128,
+  EditLocal K=32): tolerance 1e-5.
+* A bf16 decoder with head_dim 128 and 4-way grouped-query attention that
+  exercises every MFMA kernel (weight-streaming GEMM for <= 64 rows, tiled GEMM
+  above, split and unsplit attention): tolerance 2e-2.
+
+Tolerance = max |gpu - oracle| / max |oracle| per tensor group (each layer's
+repaired K rows, V rows, and the final hidden rows); slots outside P are
+compared bitwise.  The stale cache given to both sides is the oracle's own
+prefill of the original context, rounded to the model dtype.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_17983_amd as kvr
+import synth
+from oracle import decoder as od
+from oracle import select as osel
+from tests.gpu_util import TOL, Engine, OracleWeights, compare_repair, relmax, say, to_device_weights
+
+pytestmark = pytest.mark.gpu
+
+MID = synth.ModelShape("mid-bf16", 2, 512, 8, 2, 128, 1024, 2048, 1e-5, 500000.0)
+MID_BIAS = synth.scaled_shape(MID, name="mid-bf16-bias", n_heads=14, n_kv_heads=2, d_model=448, qkv_bias=True,
+                              rope_theta=1e6, rms_eps=1e-6)
+
+
+def _setup(shape, dtype, n, max_rows, seed=0, std=0.02):
+    tdt = torch.bfloat16 if dtype == kvr.KVR_BF16 else torch.float32
+    w = synth.make_weights(shape, dtype=tdt, seed=seed, std=std)
+    wd = to_device_weights(w)
+    eng = Engine(shape, wd, dtype, max_ctx=n + 64, max_rows=max_rows)
+    ow = OracleWeights(w, cache=True)
+    toks = synth.make_tokens(n, shape.vocab, seed=seed + 1)
+    return eng, ow, toks
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    shape = synth.TINY
+    eng, ow, toks = _setup(shape, kvr.KVR_F32, 512, 512)
+    new = synth.apply_edit(toks, 128, 8, shape.vocab)
+    stale_np, y_c = od.prefill(shape, ow, toks.numpy())
+    yield shape, eng, ow, toks, new, stale_np, y_c
+    eng.close()
+
+
+@pytest.fixture(scope="module")
+def mid():
+    shape = MID
+    n = 700
+    eng, ow, toks = _setup(shape, kvr.KVR_BF16, n, 700)
+    new = synth.apply_edit(toks, 300, 16, shape.vocab)
+    stale_np, _ = od.prefill(shape, ow, toks.numpy())
+    yield shape, eng, ow, toks, new, stale_np
+    eng.close()
+
+
+def _repair_case(shape, eng, ow, stale_np, new, s0, s1, positions, tag, n_cap=None):
+    tdt = eng.tdtype
+    n = new.numel()
+    n_cap = n_cap or stale_np.shape[3]
+    stale_dev = torch.zeros((shape.n_layers, 2, shape.n_kv_heads, n_cap, shape.head_dim), dtype=tdt, device="cuda")
+    stale_dev[:, :, :, :stale_np.shape[3]] = torch.from_numpy(stale_np).to(tdt).cuda()
+    ref_in = stale_dev.to(torch.float64).cpu().numpy()  # the exact values the GPU starts from
+    cache = stale_dev.clone()
+    P = od.repaired_set(s0, s1, positions)
+    hidden = torch.full((len(P), shape.d_model), float("nan"), device="cuda")
+    eng.repair([dict(cache=cache, tokens=new.cuda(), n=n, edit_start=s0, edit_end=s1, positions=positions,
+                     hidden=hidden)])
+    torch.cuda.synchronize()
+    oc = ref_in.copy()
+    y = od.repair(shape, ow, oc, new.numpy(), s0, s1, positions)
+    return compare_repair(shape, None, stale_dev, cache, hidden, oc, y, P, n, TOL[eng.dtype], tag)
+
+
+# ------------------------------------------------------------------------- tiny fp32
+
+def test_tiny_prefill(tiny):
+    shape, eng, ow, toks, new, stale_np, y_c = tiny
+    say("case: tiny fp32 prefill n=512")
+    cache = eng.new_cache(512)
+    hidden = torch.empty((512, shape.d_model), device="cuda")
+    eng.prefill(toks.cuda(), cache, hidden)
+    torch.cuda.synchronize()
+    got = cache.to(torch.float64).cpu().numpy()
+    for l in range(shape.n_layers):
+        for kv in range(2):
+            assert relmax(got[l, kv], stale_np[l, kv]) <= TOL[kvr.KVR_F32], (l, kv)
+    assert relmax(hidden.cpu().numpy(), y_c) <= TOL[kvr.KVR_F32]
+
+
+def test_tiny_repair_edit_local(tiny):
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    A = osel.select_edit_local(512, 128, 136, 32)
+    assert A == list(range(136, 168))
+    _repair_case(shape, eng, ow, stale_np, new, 128, 136, A, "tiny EditLocal K=32")
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_tiny_repair_random(tiny, seed):
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    A = osel.select_random(512, 128, 136, 32, seed)
+    _repair_case(shape, eng, ow, stale_np, new, 128, 136, A, f"tiny Random K=32 seed={seed}")
+
+
+def test_tiny_endpoint_identity(tiny):
+    """Eq. 1: recomputing all positions gives the oracle's prefill of C'."""
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    A = [p for p in range(512) if not 128 <= p < 136]
+    errs = _repair_case(shape, eng, ow, stale_np, new, 128, 136, A, "tiny endpoint")
+    oc, oy = od.prefill(shape, ow, new.numpy())
+    cache = torch.from_numpy(stale_np).float().cuda()
+    hidden = torch.empty((512, shape.d_model), device="cuda")
+    eng.repair([dict(cache=cache, tokens=new.cuda(), edit_start=128, edit_end=136, positions=A, hidden=hidden)])
+    torch.cuda.synchronize()
+    assert relmax(cache.double().cpu().numpy(), oc) <= TOL[kvr.KVR_F32]
+    assert relmax(hidden.cpu().numpy(), oy) <= TOL[kvr.KVR_F32]
+    assert errs
+
+
+def test_tiny_upstream_and_suffix(tiny):
+    """P = [s_start, n) reproduces K(C') (upstream rows cannot depend on the edit)."""
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    oc, oy = od.prefill(shape, ow, new.numpy())
+    cache = torch.from_numpy(stale_np).float().cuda()
+    hidden = torch.empty((512 - 128, shape.d_model), device="cuda")
+    eng.repair([dict(cache=cache, tokens=new.cuda(), edit_start=128, edit_end=136, positions=list(range(136, 512)),
+                     hidden=hidden)])
+    torch.cuda.synchronize()
+    assert relmax(cache.double().cpu().numpy(), oc) <= TOL[kvr.KVR_F32]
+    assert relmax(hidden.cpu().numpy(), oy[128:]) <= TOL[kvr.KVR_F32]
+
+
+def test_tiny_empty_edit_is_noop(tiny):
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    cache = torch.from_numpy(stale_np).float().cuda()
+    before = cache.clone()
+    eng.repair([dict(cache=cache, tokens=new.cuda(), edit_start=200, edit_end=200, positions=[])])
+    eng.repair([])
+    torch.cuda.synchronize()
+    assert torch.equal(cache, before)
+
+
+def test_tiny_errors_leave_cache_untouched(tiny):
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    cache = torch.from_numpy(stale_np).float().cuda()
+    before = cache.clone()
+    t = new.cuda()
+    bad = [
+        (dict(edit_start=130, edit_end=128, positions=[]), kvr.KVR_E_RANGE),
+        (dict(edit_start=128, edit_end=136, positions=[140, 139]), kvr.KVR_E_ARG),
+        (dict(edit_start=128, edit_end=136, positions=[140, 140]), kvr.KVR_E_ARG),
+        (dict(edit_start=128, edit_end=136, positions=[130]), kvr.KVR_E_ARG),
+        (dict(edit_start=128, edit_end=136, positions=[512]), kvr.KVR_E_RANGE),
+        (dict(edit_start=128, edit_end=136, positions=[-1]), kvr.KVR_E_RANGE),
+    ]
+    for kw, status in bad:
+        with pytest.raises(kvr.KvrError) as e:
+            eng.repair([dict(cache=cache, tokens=t, **kw)])
+        assert e.value.status == status, kw
+    # |P| above max_rows
+    with pytest.raises(kvr.KvrError) as e:
+        eng.repair([dict(cache=cache, tokens=t, edit_start=0, edit_end=300, positions=list(range(300, 511))),
+                    dict(cache=cache, tokens=t, edit_start=0, edit_end=2, positions=[])])
+    assert e.value.status == kvr.KVR_E_RANGE
+    # n above n_cap / max_ctx
+    with pytest.raises(kvr.KvrError) as e:
+        eng.repair([dict(cache=cache, tokens=t, n=513, edit_start=0, edit_end=1, positions=[])])
+    assert e.value.status == kvr.KVR_E_RANGE
+    with pytest.raises(kvr.KvrError):
+        kvr.kvr_prefill(eng.ctx, t.data_ptr(), 0, 512, cache.data_ptr(), None, None)
+    torch.cuda.synchronize()
+    assert torch.equal(cache, before)
+
+
+# ------------------------------------------------------------------------- mid bf16
+
+def test_mid_prefill(mid):
+    shape, eng, ow, toks, new, stale_np = mid
+    say("case: mid bf16 prefill n=700")
+    n = 700
+    cache = eng.new_cache(704)
+    hidden = torch.empty((n, shape.d_model), device="cuda")
+    eng.prefill(toks.cuda(), cache, hidden)
+    torch.cuda.synchronize()
+    got = cache.to(torch.float64).cpu().numpy()
+    errs = {}
+    for l in range(shape.n_layers):
+        for kv in range(2):
+            errs[(l, kv)] = relmax(got[l, kv, :, :n], stale_np[l, kv])
+    errs["hidden"] = relmax(hidden.cpu().numpy(), od.prefill(shape, ow, toks.numpy())[1])
+    say(f"mid prefill errors {errs}")
+    assert max(errs.values()) <= TOL[kvr.KVR_BF16]
+    assert torch.count_nonzero(cache[:, :, :, n:]) == 0
+
+
+@pytest.mark.parametrize("policy,K", [("edit_local", 32), ("edit_local", 0), ("random", 8), ("random", 128),
+                                      ("edit_local", 48)])
+def test_mid_repair(mid, policy, K):
+    shape, eng, ow, toks, new, stale_np = mid
+    A = (osel.select_edit_local(700, 300, 316, K) if policy == "edit_local"
+         else osel.select_random(700, 300, 316, K, 3))
+    _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid {policy} K={K}", n_cap=704)
+
+
+def test_mid_repair_is_idempotent_and_deterministic(mid):
+    shape, eng, ow, toks, new, stale_np = mid
+    cache = torch.from_numpy(stale_np).to(torch.bfloat16).cuda()
+    A = osel.select_random(700, 300, 316, 32, 1)
+    h1 = torch.empty((48, shape.d_model), device="cuda")
+    h2 = torch.empty_like(h1)
+    doc = dict(cache=cache, tokens=new.cuda(), edit_start=300, edit_end=316, positions=A)
+    eng.repair([dict(doc, hidden=h1)])
+    once = cache.clone()
+    eng.repair([dict(doc, hidden=h2)])
+    torch.cuda.synchronize()
+    assert torch.equal(cache, once) and torch.equal(h1, h2)
+
+
+def test_mid_batched_documents(mid):
+    """Several documents with their own caches, lengths and edits in one call."""
+    shape, eng, ow, toks, new, stale_np = mid
+    specs = [(700, 300, 316, osel.select_edit_local(700, 300, 316, 32)),
+             (700, 650, 651, osel.select_edit_local(700, 650, 651, 32)),
+             (700, 5, 9, osel.select_random(700, 5, 9, 40, 7))]
+    docs, refs = [], []
+    for i, (n, s0, s1, A) in enumerate(specs):
+        t_new = synth.apply_edit(toks, s0, s1 - s0, shape.vocab, label=i)
+        cache = torch.from_numpy(stale_np).to(torch.bfloat16).cuda()
+        ref_in = cache.to(torch.float64).cpu().numpy()
+        P = od.repaired_set(s0, s1, A)
+        hidden = torch.empty((len(P), shape.d_model), device="cuda")
+        docs.append(dict(cache=cache, tokens=t_new.cuda(), edit_start=s0, edit_end=s1, positions=A, hidden=hidden))
+        refs.append((ref_in, t_new, s0, s1, A, P, cache.clone()))
+    eng.repair(docs)
+    torch.cuda.synchronize()
+    for d, (ref_in, t_new, s0, s1, A, P, stale_dev) in zip(docs, refs):
+        oc = ref_in.copy()
+        y = od.repair(shape, ow, oc, t_new.numpy(), s0, s1, A)
+        compare_repair(shape, None, stale_dev, d["cache"], d["hidden"], oc, y, P, 700, TOL[kvr.KVR_BF16],
+                       f"mid batched span=[{s0},{s1})")
+
+
+@pytest.fixture(scope="module")
+def mid_bias():
+    shape = MID_BIAS
+    n = 333
+    eng, ow, toks = _setup(shape, kvr.KVR_BF16, n, 400, seed=5)
+    new = synth.apply_edit(toks, 100, 16, shape.vocab)
+    stale_np, _ = od.prefill(shape, ow, toks.numpy())
+    yield shape, eng, ow, toks, new, stale_np
+    eng.close()
+
+
+@pytest.mark.parametrize("K", [32, 200])
+def test_mid_bias_gqa7_repair(mid_bias, K):
+    """QKV bias and 7 query heads per kv head (the Qwen2.5 arrangement)."""
+    shape, eng, ow, toks, new, stale_np = mid_bias
+    A = osel.select_edit_local(333, 100, 116, K)
+    _repair_case(shape, eng, ow, stale_np, new, 100, 116, A, f"mid-bias K={K}")
