@@ -11,9 +11,10 @@ timed for the speedup.
 
 Prints one JSON line: ms per repair (value), algorithmic HBM GB/s, recomputed
 tokens/s, prefill ms and speedup, the roofline of the dominant kernel (the
-gate/up projection with SwiGLU, launched through kvr_linear with the exact
-repair launch configuration and timed with HIP events on its stream), and the
-fp64 CPU oracle's time on a bounded sample of the same repair.
+gate/up projection with SwiGLU, timed inside the repair with HIP events the
+library records on the call's stream after every launch), a per-step
+breakdown, and the fp64 CPU oracle's time on a bounded sample of the same
+repair.
 """
 from __future__ import annotations
 
@@ -46,7 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b-k32", choices=sorted(WORKLOADS))
     ap.add_argument("--prefill-steps", type=int, default=5)
-    ap.add_argument("--kernel-iters", type=int, default=64)
+    ap.add_argument("--profile-steps", type=int, default=5,
+                    help="repairs run with per-launch event profiling after the timed loop")
     ap.add_argument("--cpu-layers", type=int, default=8,
                     help="layers of the repair the CPU oracle runs for its bounded sample")
     ap.add_argument("--no-cpu", action="store_true")
@@ -140,28 +142,22 @@ def main():
     log(f"prefill: median {prefill_ms:.2f} ms")
     del pcache
 
-    # ---- dominant kernel: gate/up projection + SwiGLU at R rows, cycling layers so
-    # that no launch finds its weights in the last-level cache
-    x = torch.randn((R, shape.d_model), device=dev).to(torch.bfloat16)
-    a_out = torch.empty((R, shape.d_ffn), dtype=torch.bfloat16, device=dev)
+    # ---- per-step breakdown and the dominant kernel (gate/up + SwiGLU), timed in
+    # the repair itself: HIP events recorded by the library on this stream after
+    # every launch, over a separate profiled loop of the same repair
+    kvr.kvr_profile_enable(ctx, True)
+    kvr.kvr_profile_read(ctx)
+    for _ in range(args.profile_steps):
+        kvr.kvr_repair(ctx, [doc], stream.cuda_stream)
+    prof = kvr.kvr_profile_read(ctx)
+    kvr.kvr_profile_enable(ctx, False)
     L = shape.n_layers
-    for l in range(L):
-        lw = w["layers"][l]
-        kvr.kvr_linear(ctx, kvr.KVR_EPI_SWIGLU, x.data_ptr(), R, shape.d_model, lw["w_gate"].data_ptr(),
-                       lw["w_up"].data_ptr(), shape.d_ffn, a_out.data_ptr(), stream.cuda_stream)
-    torch.cuda.synchronize()
-    k0 = torch.cuda.Event(enable_timing=True)
-    k1 = torch.cuda.Event(enable_timing=True)
-    k0.record(stream)
-    for i in range(args.kernel_iters):
-        lw = w["layers"][i % L]
-        kvr.kvr_linear(ctx, kvr.KVR_EPI_SWIGLU, x.data_ptr(), R, shape.d_model, lw["w_gate"].data_ptr(),
-                       lw["w_up"].data_ptr(), shape.d_ffn, a_out.data_ptr(), stream.cuda_stream)
-    k1.record(stream)
-    torch.cuda.synchronize()
-    kern_ms = k0.elapsed_time(k1) / args.kernel_iters
+    steps_ms = {k: round(v[0] / args.profile_steps, 4) for k, v in prof.items() if v[1]}
+    gu_ms, gu_n = prof["gate_up_swiglu"]
+    kern_ms = gu_ms / gu_n
     kern_bytes = 2 * shape.d_ffn * shape.d_model * 2 + R * shape.d_model * 2 + R * shape.d_ffn * 2
     kern_gbs = kern_bytes / (kern_ms * 1e-3) / 1e9
+    log(f"per-step ms per repair: {steps_ms}")
     log(f"gate/up+SwiGLU kernel: {kern_ms * 1e3:.1f} us/launch, {kern_gbs:.0f} GB/s")
 
     traffic = None
@@ -204,6 +200,7 @@ def main():
         "prefill_ms": round(prefill_ms, 3),
         "speedup_vs_prefill": round(prefill_ms / ms, 2),
         "token_layer_proxy_speedup": round(n / R, 2),
+        "steps_ms_per_repair": steps_ms,
         "roofline": {"kernel": "gate/up projection + SwiGLU (linear_skinny_kernel, SWIGLU epilogue)",
                      "bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(kern_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,

@@ -167,23 +167,24 @@ typedef enum { KVR_EDIT_LOCAL = 0, KVR_RANDOM = 1 } kvr_policy;
 kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_start, int32_t edit_end,
                       int32_t K, uint64_t seed, int32_t *h_out, int32_t *n_out);
 
-typedef enum { KVR_EPI_STORE = 0, KVR_EPI_ADD = 1, KVR_EPI_SWIGLU = 2 } kvr_epilogue;
+/* Per-step GPU time accounting, a tracing aid for benchmarks.  While enabled
+ * (it is off after kvr_create), every kernel launch of a prefill or repair
+ * pass is followed by a HIP event recorded on the call's stream, tagged with
+ * the step of the layer loop it belongs to ("embed", "rmsnorm", "qkv_proj",
+ * "rope_scatter", "attention", "attention_combine", "o_proj",
+ * "gate_up_swiglu", "down_proj", "final_norm").  The time of a launch is the
+ * elapsed time from the previous event of its pass to its own event (kernel
+ * duration plus the gap before it).  Enabling adds one event per launch.
+ * Errors: KVR_E_ARG (NULL context). */
+kvr_status kvr_profile_enable(kvr_ctx *ctx, int32_t enable);
 
-/* One projection of the decoder exactly as the prefill and repair passes run
- * it (same kernel choice and launch configuration for this shape), exposed
- * for kernel benchmarks and tests.  Y = X W^T with X [rows][in_features] and
- * W [out_features][in_features], both in the context's dtype, row-major,
- * 16-byte aligned:
- *   KVR_EPI_STORE:  d_out fp32 [rows][out_features] = Y
- *   KVR_EPI_ADD:    d_out fp32 [rows][out_features] += Y (the residual add)
- *   KVR_EPI_SWIGLU: d_out (dtype) [rows][out_features] = silu(X W^T) * (X W2^T),
- *                   the SwiGLU MLP input; d_w = gate, d_w2 = up.
- * d_w2 must be NULL unless SWIGLU.  1 <= rows <= the context's row capacity
- * (max(max_rows, min(max_ctx, 8192))).  Uses the context's split-K scratch,
- * so it is ordered with the context's other calls.
- * Errors: KVR_E_ARG (NULL/misaligned pointers, bad epilogue), KVR_E_RANGE. */
-kvr_status kvr_linear(kvr_ctx *ctx, kvr_epilogue epilogue, const void *d_x, int32_t rows, int32_t in_features,
-                      const void *d_w, const void *d_w2, int32_t out_features, void *d_out, void *stream);
+/* Wait for the recorded events, add their times to per-step totals and report
+ * them: for i < min(*n_steps, capacity), names[i] (static strings), total_ms[i]
+ * and launches[i] accumulated since the previous read; the totals are then
+ * cleared.  *n_steps receives the number of steps.  Errors: KVR_E_ARG (NULL
+ * context, n_steps or, when capacity > 0, output arrays), KVR_E_HIP. */
+kvr_status kvr_profile_read(kvr_ctx *ctx, int32_t capacity, const char **names, double *total_ms,
+                            int64_t *launches, int32_t *n_steps);
 
 /* Text of the last failure on this context, or of the last failed
  * kvr_create/kvr_select when ctx is NULL.  Never NULL; valid until the next

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_float, c_int, c_int32, c_size_t, c_uint64, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int, c_int32, c_int64, c_size_t, c_uint64, c_void_p
 from typing import Optional, Sequence
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvr.so")
@@ -22,10 +22,8 @@ KVR_EDIT_LOCAL, KVR_RANDOM = 0, 1
 STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPORTED", 4: "KVR_E_NOMEM",
                 5: "KVR_E_HIP"}
 
-KVR_EPI_STORE, KVR_EPI_ADD, KVR_EPI_SWIGLU = 0, 1, 2
-
 EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
-            "kvr_select", "kvr_linear", "kvr_last_error")
+            "kvr_select", "kvr_profile_enable", "kvr_profile_read", "kvr_last_error")
 
 
 class KvrError(RuntimeError):
@@ -85,9 +83,11 @@ def load() -> ctypes.CDLL:
     lib.kvr_repair.restype = c_int
     lib.kvr_select.argtypes = [c_int, c_int32, c_int32, c_int32, c_int32, c_uint64, POINTER(c_int32), POINTER(c_int32)]
     lib.kvr_select.restype = c_int
-    lib.kvr_linear.argtypes = [c_void_p, c_int, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
-                               c_void_p]
-    lib.kvr_linear.restype = c_int
+    lib.kvr_profile_enable.argtypes = [c_void_p, c_int32]
+    lib.kvr_profile_enable.restype = c_int
+    lib.kvr_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_char_p), POINTER(c_double), POINTER(c_int64),
+                                     POINTER(c_int32)]
+    lib.kvr_profile_read.restype = c_int
     lib.kvr_last_error.argtypes = [c_void_p]
     lib.kvr_last_error.restype = c_char_p
     _lib = lib
@@ -142,9 +142,19 @@ def kvr_repair(ctx: int, docs: Sequence[kvr_doc], stream: Optional[int] = None) 
     _check(load().kvr_repair(ctx, arr, len(docs), stream), ctx)
 
 
-def kvr_linear(ctx: int, epilogue: int, d_x: int, rows: int, in_features: int, d_w: int, d_w2: Optional[int],
-               out_features: int, d_out: int, stream: Optional[int] = None) -> None:
-    _check(load().kvr_linear(ctx, epilogue, d_x, rows, in_features, d_w, d_w2, out_features, d_out, stream), ctx)
+def kvr_profile_enable(ctx: int, enable: bool = True) -> None:
+    _check(load().kvr_profile_enable(ctx, 1 if enable else 0), ctx)
+
+
+def kvr_profile_read(ctx: int) -> dict:
+    """{step name: (total ms, launches)} accumulated since the previous read."""
+    cap = 32
+    names = (c_char_p * cap)()
+    ms = (c_double * cap)()
+    cnt = (c_int64 * cap)()
+    n = c_int32(0)
+    _check(load().kvr_profile_read(ctx, cap, names, ms, cnt, ctypes.byref(n)), ctx)
+    return {names[i].decode(): (ms[i], cnt[i]) for i in range(min(n.value, cap))}
 
 
 def kvr_select(policy: int, n: int, edit_start: int, edit_end: int, K: int, seed: int = 0) -> list:

@@ -1,18 +1,29 @@
 // Causal grouped-query attention of a set of rows over a KV cache, bf16 MFMA,
 // head_dim 128.
 //
-// A work item is (document, kv head, up to 16 consecutive rows of that
-// document, key range [k0, k1)).  The G = Hq/Hkv query heads that share the kv
-// head each form one 16-row MFMA tile, so one K/V tile staged in LDS serves
-// 16*G query rows.  Per 64-key tile: S = Q K^T (v_mfma_f32_16x16x32_bf16, K
-// row-major in LDS), causal mask against each row's own position, online
-// softmax in the exp2 domain (row max / sum over the 16 lanes of a row group
-// by cross-lane shuffles), P rounded to bf16 and re-read from LDS in operand
-// layout, O += P V with V stored transposed in LDS.  When the key range of a
-// row block is split over several items (few rows, long contexts) each item
+// A work item is (document, kv head, up to 16*MT consecutive rows of that
+// document, key range [k0, k1)).  The G = Hq/Hkv query heads sharing the kv
+// head times the item's 16-row tiles give (head, row tile) pairs, dealt
+// round-robin to the eight wavefronts of the block (two per SIMD); every
+// 64-key K/V tile staged in LDS serves all of them, so the cache is read once
+// per item.  Scores are computed transposed, S^T = K Q^T
+// (v_mfma_f32_16x16x32_bf16 with the key tile as A operand), so that each lane
+// owns one query row: the row max and sum of a tile are 16 in-lane values plus
+// two cross-lane steps.  The probabilities go straight from the S^T
+// accumulator into the B operand of O^T += V^T P^T: both operands enumerate the
+// 32 keys of a k-step in the same permuted order (slot j of lane group g <->
+// key 16*(j/4) + 4*g + j%4), so P never leaves registers; V is stored
+// transposed in LDS.  Softmax runs in the exp2 domain; the running max is only
+// raised (and the accumulators rescaled) when a row's tile max exceeds it by
+// more than 2^8, which keeps every probability below 256.  The causal mask is
+// applied only on tiles that reach a row's own position.  The next K/V tile is
+// fetched into registers while the current one is used.  When the key range of
+// a row block is split over several items (few rows, long contexts) each item
 // writes (m, l, unnormalised O) partials and a combine pass merges them with
-// the usual log-sum-exp rescaling.
+// log-sum-exp rescaling.
 #include <math.h>
+
+#include <algorithm>
 
 #include "common.h"
 
@@ -22,236 +33,284 @@ namespace {
 
 constexpr int HD = ATT_HD;
 constexpr int KT = ATT_KT;
+constexpr int WAVES = 8;           // wavefronts per block
+constexpr int NLD = 16 / WAVES;    // 16-byte K (and V) loads per thread per tile
 constexpr int KS_STRIDE = HD + 8;  // keys tile row stride (bf16)
 constexpr int VT_STRIDE = KT + 8;  // transposed values row stride (bf16)
-constexpr int PS_STRIDE = KT + 8;
-constexpr int MAXH = 2;            // query heads per wavefront (G <= 8)
 constexpr int PART_ROW = HD + 4;   // floats per (head, row) partial: O[128], m, l
+constexpr float RESCALE_SLACK = 8.0f;  // log2 headroom before the running max is raised
 
-__device__ __forceinline__ bf16x8 lds16(const bf16_t *p) { return *reinterpret_cast<const bf16x8 *>(p); }
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
 
-__device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+__device__ __forceinline__ bf16x8 ld16(const bf16_t *p) { return *reinterpret_cast<const bf16x8 *>(p); }
+
+// reductions over the four lanes l, l^16, l^32, l^48 that hold one query row
+__device__ __forceinline__ float xmax4(float v) {
+    v = fmaxf(v, __shfl_xor(v, 16, 64));
+    return fmaxf(v, __shfl_xor(v, 32, 64));
 }
-__device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-    return v;
+__device__ __forceinline__ float xsum4(float v) {
+    v += __shfl_xor(v, 16, 64);
+    return v + __shfl_xor(v, 32, 64);
 }
 
-__global__ __launch_bounds__(256) void attention_mfma_kernel(const bf16_t *Q, const RowInfo *rows,
-                                                             const DocInfo *docs, const AttnItem *items, int layer,
-                                                             int Hq, int Hkv, float *part, bf16_t *O) {
+// PPW: (head, row tile) pairs per wavefront; MT: row tiles of a full item.
+template <int PPW>
+__global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t *Q, const RowInfo *rows,
+                                                                    const DocInfo *docs, const AttnItem *items,
+                                                                    int layer, int Hq, int Hkv, int MT, float *part,
+                                                                    bf16_t *O, int o_perm) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS_STRIDE];
     __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * VT_STRIDE];
-    __shared__ __attribute__((aligned(16))) bf16_t Ps[4][16 * PS_STRIDE];
 
     const AttnItem it = items[blockIdx.x];
     const DocInfo dc = docs[it.doc];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront index (uniform)
     const int G = Hq / Hkv;
     const int qd = Hq * HD;
+    const int MTi = (it.nrows + 15) >> 4;  // row tiles this item has
+    const int npairs = G * MTi;
     const size_t head_stride = (size_t)dc.n_cap * HD;
     const bf16_t *Kg = (const bf16_t *)dc.cache + (((size_t)layer * 2 + 0) * Hkv + it.kvh) * head_stride;
     const bf16_t *Vg = (const bf16_t *)dc.cache + (((size_t)layer * 2 + 1) * Hkv + it.kvh) * head_stride;
 
-    // rows 4*(lane/16)+e of the accumulator tiles: their positions (-1 = padding)
-    int prow[4];
+    // this wavefront's pairs: p = w + WAVES*i -> head t = p / MTi, row tile p % MTi
+    bool pvalid[PPW];
+    int pt[PPW], pm[PPW], prow[PPW];
+    bf16x8 qv[PPW][4];
+    f32x4 oacc[PPW][8];
+    float m[PPW], l[PPW];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = 4 * (lane >> 4) + e;
-        prow[e] = i < it.nrows ? rows[it.row0 + i].pos : -1;
-    }
-
-    // Q operands of this wavefront's heads: lane holds row lane%16, dims 32*ks + 8*(lane/16)
-    const int qrow = it.row0 + min(lane & 15, it.nrows - 1);
-    bf16x8 qv[MAXH][4];
-    bool hvalid[MAXH];
+    for (int i = 0; i < PPW; ++i) {
+        const int p = w + WAVES * i;
+        pvalid[i] = p < npairs;
+        pt[i] = pvalid[i] ? p / MTi : 0;
+        pm[i] = pvalid[i] ? p % MTi : 0;
+        const int r = pm[i] * 16 + (lane & 15);  // this lane's query row within the item
+        prow[i] = (pvalid[i] && r < it.nrows) ? rows[it.row0 + r].pos : -1;
+        const int qrow = it.row0 + min(r, it.nrows - 1);
+        const int j = it.kvh * G + pt[i];
 #pragma unroll
-    for (int h = 0; h < MAXH; ++h) {
-        const int t = w + 4 * h;
-        hvalid[h] = t < G;
-        const int j = it.kvh * G + (hvalid[h] ? t : 0);
+        for (int ks = 0; ks < 4; ++ks) qv[i][ks] = ld16(Q + (size_t)qrow * qd + j * HD + ks * 32 + 8 * g);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-            qv[h][ks] = lds16(Q + (size_t)qrow * qd + j * HD + ks * 32 + 8 * (lane >> 4));
-    }
-
-    f32x4 oacc[MAXH][8];
-    float m[MAXH][4], l[MAXH][4];
-#pragma unroll
-    for (int h = 0; h < MAXH; ++h) {
-#pragma unroll
-        for (int nt = 0; nt < 8; ++nt) oacc[h][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { m[h][e] = -INFINITY; l[h][e] = 0.f; }
+        for (int nt = 0; nt < 8; ++nt) oacc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        m[i] = -INFINITY;
+        l[i] = 0.f;
     }
     const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
+    const int minpos = rows[it.row0].pos;  // rows ascend: every row sees all keys <= minpos
 
+    // the next key tile is fetched into registers while the current one is used
+    u32x4 kreg[NLD], vreg[NLD];
+#define KVR_ATT_FETCH(kt_)                                                                                  \
+    _Pragma("clang loop unroll(full)") for (int i = 0; i < NLD; ++i) {                                     \
+        /* K: key (tid + 64*WAVES*i)/16, dims (tid%16)*8; V: key tid%64, dims 8*(tid/64 + WAVES*i) */       \
+        const int ksrc = min((kt_) + ((tid + 64 * WAVES * i) >> 4), it.k1 - 1);                             \
+        kreg[i] = *reinterpret_cast<const u32x4 *>(Kg + (size_t)ksrc * HD + (tid & 15) * 8);                \
+        const int vsrc = min((kt_) + (tid & 63), it.k1 - 1);                                                \
+        vreg[i] = *reinterpret_cast<const u32x4 *>(Vg + (size_t)vsrc * HD + 8 * ((tid >> 6) + WAVES * i));  \
+    }
+    KVR_ATT_FETCH(it.k0)
     for (int kt = it.k0; kt < it.k1; kt += KT) {
         __syncthreads();
-        // K tile: thread covers keys tid/16 + 16*i, dims (tid%16)*8 .. +8
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int key = (tid >> 4) + 16 * i;
-            const int src = min(kt + key, it.k1 - 1);
-            const uint4 u = *reinterpret_cast<const uint4 *>(Kg + (size_t)src * HD + (tid & 15) * 8);
-            *reinterpret_cast<uint4 *>(&Ks[key * KS_STRIDE + (tid & 15) * 8]) = u;
-        }
-        // V tile, stored transposed: thread covers key tid%64, dims 8*(tid/64 + 4*i) .. +8
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int key = tid & 63;
-            const int d0 = 8 * ((tid >> 6) + 4 * i);
-            const int src = min(kt + key, it.k1 - 1);
-            const uint4 u = *reinterpret_cast<const uint4 *>(Vg + (size_t)src * HD + d0);
-            const bf16_t *pv = reinterpret_cast<const bf16_t *>(&u);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) Vt[(d0 + e) * VT_STRIDE + key] = pv[e];
-        }
-        __syncthreads();
-
-#pragma unroll
-        for (int h = 0; h < MAXH; ++h) {
-            if (!hvalid[h]) continue;  // uniform per wavefront
-            f32x4 s[4];
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                s[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const bf16x8 kb = lds16(&Ks[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * (lane >> 4)]);
-                    s[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qv[h][ks], kb, s[nt], 0, 0, 0);
-                }
-            }
-            // mask + scale; per-row max over the tile
-            float mx[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) mx[e] = -INFINITY;
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                const int key = kt + nt * 16 + (lane & 15);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bool ok = key < it.k1 && key <= prow[e];
-                    const float v = ok ? s[nt][e] * sc : -INFINITY;
-                    s[nt][e] = v;
-                    mx[e] = fmaxf(mx[e], v);
-                }
-            }
-            float corr[4];
+#pragma clang loop unroll(full)
+        for (int i = 0; i < NLD; ++i) {
+            *reinterpret_cast<u32x4 *>(&Ks[((tid + 64 * WAVES * i) >> 4) * KS_STRIDE + (tid & 15) * 8]) = kreg[i];
+            const int d0 = 8 * ((tid >> 6) + WAVES * i);
+            const unsigned int wv[4] = {vreg[i][0], vreg[i][1], vreg[i][2], vreg[i][3]};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float mt = group16_max(mx[e]);
-                const float mnew = fmaxf(m[h][e], mt);
-                const float muse = mnew == -INFINITY ? 0.f : mnew;
-                corr[e] = exp2f(m[h][e] - muse);
-                m[h][e] = mnew;
-                float rs = 0.f;
-#pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const float p = exp2f(s[nt][e] - muse);
-                    s[nt][e] = p;
-                    rs += p;
-                }
-                l[h][e] = l[h][e] * corr[e] + group16_sum(rs);
+                Vt[(d0 + 2 * e) * VT_STRIDE + (tid & 63)] = (bf16_t)(wv[e] & 0xffffu);
+                Vt[(d0 + 2 * e + 1) * VT_STRIDE + (tid & 63)] = (bf16_t)(wv[e] >> 16);
             }
+        }
+        __syncthreads();
+        if (kt + KT < it.k1) {
+            KVR_ATT_FETCH(kt + KT)
+        }
+        const bool full = kt + KT <= it.k1 && kt + KT - 1 <= minpos;  // no key of the tile is masked
+
+        // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the tile
+        f32x4 s[PPW][4];
 #pragma unroll
-            for (int nt = 0; nt < 8; ++nt)
+        for (int nt = 0; nt < 4; ++nt) {
+            bf16x8 kb[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) oacc[h][nt][e] *= corr[e];
-            // P (bf16) -> LDS, row-major [16 rows][64 keys]
-            bf16_t *ps = Ps[w];
+            for (int ks = 0; ks < 4; ++ks) kb[ks] = ld16(&Ks[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (!pvalid[i]) continue;
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks], qv[i][ks], s[i][nt], 0, 0, 0);
+            }
+        }
+        // online softmax, one query row per lane column
+        bf16x8 pb[PPW][2];
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) {
+            if (!pvalid[i]) continue;
+            float mx = -INFINITY;
+            if (full) {
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[i][nt][e]);
+            } else {
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int key = kt + nt * 16 + 4 * g + e;
+                        const float v = (key < it.k1 && key <= prow[i]) ? s[i][nt][e] : -INFINITY;
+                        s[i][nt][e] = v;
+                        mx = fmaxf(mx, v);
+                    }
+            }
+            mx = xmax4(mx) * sc;
+            if (__any(mx > m[i] + RESCALE_SLACK)) {
+                const float mnew = fmaxf(m[i], mx);
+                const float corr = m[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[i] - mnew);
+                m[i] = mnew;
+                l[i] *= corr;
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt) oacc[i][nt] *= corr;
+            }
+            const float muse = m[i] == -INFINITY ? 0.f : m[i];
+            float rs = 0.f;
 #pragma unroll
             for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    ps[(4 * (lane >> 4) + e) * PS_STRIDE + nt * 16 + (lane & 15)] = f32_to_bf16(s[nt][e]);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            bf16x8 pa[2];
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) pa[ks] = lds16(&ps[(lane & 15) * PS_STRIDE + ks * 32 + 8 * (lane >> 4)]);
-#pragma unroll
-            for (int nt = 0; nt < 8; ++nt)
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const bf16x8 vb = lds16(&Vt[(nt * 16 + (lane & 15)) * VT_STRIDE + ks * 32 + 8 * (lane >> 4)]);
-                    oacc[h][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[ks], vb, oacc[h][nt], 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    const float p = __builtin_amdgcn_exp2f(s[i][nt][e] * sc - muse);
+                    s[i][nt][e] = p;
+                    rs += p;
                 }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            l[i] += xsum4(rs);
+            // B operand P^T for 32-key step ks: slot j <-> key 32*ks + 16*(j/4) + 4*g + j%4
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                u32x4 u;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x2 f = {s[i][2 * ks + q / 2][2 * (q % 2)], s[i][2 * ks + q / 2][2 * (q % 2) + 1]};
+                    u[q] = __builtin_bit_cast(unsigned int, __builtin_convertvector(f, bf16x2));
+                }
+                pb[i][ks] = __builtin_bit_cast(bf16x8, u);
+            }
+        }
+        // O^T += V^T P^T: A operand = V^T rows (dims 16*nt + lane%16) over the same key slots
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) {
+            bf16x8 va[2];
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16_t *vr = &Vt[(nt * 16 + (lane & 15)) * VT_STRIDE + ks * 32 + 4 * g];
+                const uint2 lo = *reinterpret_cast<const uint2 *>(vr);
+                const uint2 hi = *reinterpret_cast<const uint2 *>(vr + 16);
+                const u32x4 u = {lo.x, lo.y, hi.x, hi.y};
+                va[ks] = __builtin_bit_cast(bf16x8, u);
+            }
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                if (!pvalid[i]) continue;
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks], pb[i][ks], oacc[i][nt], 0, 0, 0);
+            }
         }
     }
+#undef KVR_ATT_FETCH
 
-    // write out: accumulator rows 4*(lane/16)+e, dims nt*16 + lane%16
+    // O^T accumulator: lane holds query row lane%16, dims 16*nt + 4*g + e
+    const int rows_item = 16 * MT;
 #pragma unroll
-    for (int h = 0; h < MAXH; ++h) {
-        if (!hvalid[h]) continue;
-        const int t = w + 4 * h;
+    for (int i = 0; i < PPW; ++i) {
+        if (!pvalid[i]) continue;
+        const int ri = pm[i] * 16 + (lane & 15);
+        if (ri >= it.nrows) continue;
+        const int t = pt[i];
         const int j = it.kvh * G + t;
+        if (it.part < 0) {
+            const float inv = 1.0f / l[i];
+            const int r = it.row0 + ri;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int i = 4 * (lane >> 4) + e;
-            if (i >= it.nrows) continue;
-            if (it.part < 0) {
-                const float inv = 1.0f / l[h][e];
-                bf16_t *o = O + (size_t)(it.row0 + i) * qd + j * HD + (lane & 15);
-#pragma unroll
-                for (int nt = 0; nt < 8; ++nt) o[nt * 16] = f32_to_bf16(oacc[h][nt][e] * inv);
-            } else {
-                float *p = part + ((size_t)(it.part * G + t) * 16 + i) * PART_ROW;
-#pragma unroll
-                for (int nt = 0; nt < 8; ++nt) p[nt * 16 + (lane & 15)] = oacc[h][nt][e];
-                if ((lane & 15) == 0) { p[HD] = m[h][e]; p[HD + 1] = l[h][e]; }
+            for (int nt = 0; nt < 8; ++nt) {
+                const int c = j * HD + nt * 16 + 4 * g;  // 4 consecutive columns, 8-byte aligned
+                const f32x2 a = {oacc[i][nt][0] * inv, oacc[i][nt][1] * inv};
+                const f32x2 b = {oacc[i][nt][2] * inv, oacc[i][nt][3] * inv};
+                const uint2 v = make_uint2(__builtin_bit_cast(unsigned int, __builtin_convertvector(a, bf16x2)),
+                                           __builtin_bit_cast(unsigned int, __builtin_convertvector(b, bf16x2)));
+                *reinterpret_cast<uint2 *>(O + (o_perm ? perm_offset(r, c, qd) : (size_t)r * qd + c)) = v;
             }
+        } else {
+            float *p = part + ((size_t)(it.part * G + t) * rows_item + ri) * PART_ROW;
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) *reinterpret_cast<f32x4 *>(p + nt * 16 + 4 * g) = oacc[i][nt];
+            if (g == 0) { p[HD] = m[i]; p[HD + 1] = l[i]; }
         }
     }
 }
 
-// One block per (combine item, query head of the group): merge the split
-// partials of up to 16 rows.
+// One block per (combine item, query head of the group, row): merge the split
+// partials of one row in a single pass with running max rescaling (exp2 domain).
 __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
-                                                                int Hkv, bf16_t *O) {
+                                                                int Hkv, int MT, bf16_t *O, int o_perm) {
     const CombineItem it = items[blockIdx.x];
-    const int t = blockIdx.y;
+    const int t = blockIdx.y, i = blockIdx.z;
+    if (i >= it.nrows) return;
     const int G = Hq / Hkv;
+    const int rows_item = 16 * MT;
     const int j = it.kvh * G + t;
     const int d = threadIdx.x;  // 0..127
-    for (int i = 0; i < it.nrows; ++i) {
-        float M = -INFINITY;
-        for (int q = 0; q < it.nparts; ++q)
-            M = fmaxf(M, part[((size_t)((it.part0 + q) * G + t) * 16 + i) * PART_ROW + HD]);
-        float L = 0.f, acc = 0.f;
-        for (int q = 0; q < it.nparts; ++q) {
-            const float *p = part + ((size_t)((it.part0 + q) * G + t) * 16 + i) * PART_ROW;
-            const float mq = p[HD];
-            const float f = mq == -INFINITY ? 0.f : exp2f(mq - M);
-            L += p[HD + 1] * f;
-            acc += p[d] * f;
-        }
-        O[(size_t)(it.row0 + i) * Hq * HD + j * HD + d] = f32_to_bf16(acc / L);
+    float M = -INFINITY, L = 0.f, acc = 0.f;
+    for (int q = 0; q < it.nparts; ++q) {
+        const float *p = part + ((size_t)((it.part0 + q) * G + t) * rows_item + i) * PART_ROW;
+        const float mq = p[HD], lq = p[HD + 1], oq = p[d];
+        if (mq == -INFINITY) continue;
+        const float Mn = fmaxf(M, mq);
+        const float a = exp2f(M - Mn), b = exp2f(mq - Mn);
+        acc = acc * a + oq * b;
+        L = L * a + lq * b;
+        M = Mn;
     }
+    const int r = it.row0 + i, c = j * HD + d;
+    O[o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c] = f32_to_bf16(acc / L);
 }
 
 }  // namespace
 
+int attention_row_tiles(int Hq, int Hkv) {
+    const int G = Hq / Hkv;
+    return G >= 16 ? 1 : std::min(4, std::max(1, 16 / G));
+}
+
 hipError_t launch_attention_mfma(const bf16_t *Q, const RowInfo *rows, const DocInfo *docs, const AttnItem *items,
-                                 int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O, hipStream_t s) {
+                                 int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O, bool o_perm,
+                                 hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
-    hipLaunchKernelGGL(attention_mfma_kernel, dim3(n_items), dim3(256), 0, s, Q, rows, docs, items, layer, Hq, Hkv,
-                       part, O);
+    const int MT = attention_row_tiles(Hq, Hkv);
+    const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
+    if (ppw == 1)
+        hipLaunchKernelGGL(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, rows, docs, items, layer,
+                           Hq, Hkv, MT, part, O, (int)o_perm);
+    else if (ppw == 2)
+        hipLaunchKernelGGL(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, rows, docs, items, layer,
+                           Hq, Hkv, MT, part, O, (int)o_perm);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq, int Hkv,
-                                    bf16_t *O, hipStream_t s) {
+                                    bf16_t *O, bool o_perm, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
-    hipLaunchKernelGGL(attention_combine_kernel, dim3(n_items, Hq / Hkv), dim3(128), 0, s, items, part, Hq, Hkv, O);
+    const int MT = attention_row_tiles(Hq, Hkv);
+    hipLaunchKernelGGL(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
+                       Hkv, MT, O, (int)o_perm);
     return hipGetLastError();
 }
 

@@ -10,6 +10,15 @@ typedef uint16_t bf16_t;  // raw bf16 bits in memory
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+// "Operand order" of an activation matrix [rows][K] (rows padded to a multiple
+// of 16, K a multiple of 32): the 16-byte A operand of v_mfma_f32_16x16x32_bf16
+// for 16-row tile t and k-step s (32 columns) is stored for the 64 lanes
+// contiguously, lane l holding row 16t + l%16, columns 32s + 8*(l/16) .. +8.
+__host__ __device__ __forceinline__ size_t perm_offset(int r, int c, int K) {
+    return ((size_t)((r >> 4) * (K >> 5) + (c >> 5)) * 64 + (r & 15) + 16 * ((c & 31) >> 3)) * 8 + (c & 7);
+}
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
@@ -86,33 +95,52 @@ struct LinearArgs {
     int32_t *counters;    // split-K tile counters (kept at zero between calls)
 };
 
+// Skinny (R <= 64) linear layer: X in operand order; STORE writes fp32 partial
+// tiles [split][R][N]; SWIGLU (split 1) writes silu(gate)*up in operand order.
+struct SkinnyArgs {
+    const void *x;
+    int32_t R, K, N;      // N: output columns (SWIGLU: number of features)
+    const void *w[3];
+    int32_t seg_end[3];
+    void *out;
+    int32_t split;
+};
+
 // ---- launchers (each enqueues on `stream`; return hipSuccess or the launch error)
 
 hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int R, const void *embed,
                         int d, int vocab, float *H, hipStream_t s);
-hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, const float *H, const void *gain, int R, int d,
-                          float eps, void *X, int ldx, hipStream_t s);
-hipError_t launch_final_norm(bool bf16_gain, const float *H, const void *gain, const RowInfo *rows,
-                             const DocInfo *docs, int R, int d, float eps, hipStream_t s);
-hipError_t launch_rope_scatter(bool bf16, const float *qkv, const void *bq, const void *bk, const void *bv,
-                               const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq, int Hkv,
-                               int hd, const float *rope_cos, const float *rope_sin, void *Q, hipStream_t s);
+// RMSNorm of the residual rows.  First H[r] += sum of `nsplit` fp32 partial
+// tiles part[s][R][d] (the split-K outputs of the projection that produced the
+// residual update; nsplit 0 = none), then X = H * rsqrt(mean(H^2)+eps) * gain,
+// row-major with stride ldx, or in operand order when `perm`.
+hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
+                          int R, int d, float eps, void *X, int ldx, bool perm, hipStream_t s);
+hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
+                             const RowInfo *rows, const DocInfo *docs, int R, int d, float eps, hipStream_t s);
+// qkv: `nsplit` fp32 tiles [nsplit][R][qd+2kd] summed in order.
+hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const void *bq, const void *bk,
+                               const void *bv, const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq,
+                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q,
+                               hipStream_t s);
+// O is written row-major [R][Hq*hd], or in operand order when o_perm.
 hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
-                                   int layer, int Hq, int Hkv, int hd, void *O, hipStream_t s);
+                                   int layer, int Hq, int Hkv, int hd, void *O, bool o_perm, hipStream_t s);
+// 16-row tiles per attention work item for a head grouping (items carry up to
+// 16 * this many rows).
+int attention_row_tiles(int Hq, int Hkv);
 hipError_t launch_attention_mfma(const bf16_t *Q, const RowInfo *rows, const DocInfo *docs,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
-                                 float *part, bf16_t *O, hipStream_t s);
+                                 float *part, bf16_t *O, bool o_perm, hipStream_t s);
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
-                                    int Hkv, bf16_t *O, hipStream_t s);
+                                    int Hkv, bf16_t *O, bool o_perm, hipStream_t s);
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
-// Skinny MFMA path (R <= 64): split = cross-block split-K factor, nt = 16-row
-// weight tiles per wave (2 or 4).
-hipError_t launch_linear_skinny(int epi, const LinearArgs &a, int split, int nt, hipStream_t s);
+// Skinny MFMA path (R <= 64); nt = 16-row weight tiles per wave (1, 2 or 4).
+hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s);
 // Tiled MFMA path for many rows.
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
 
 // Attention item geometry shared by the planner and the kernels.
-constexpr int ATT_ROWS = 16;   // query positions per item
 constexpr int ATT_KT = 64;     // keys per LDS tile
 constexpr int ATT_HD = 128;    // head_dim of the MFMA attention kernel
 

@@ -42,13 +42,9 @@ struct kvr_ctx {
 
     char *ws = nullptr;
     size_t ws_bytes = 0;
-    float *H = nullptr, *QKV = nullptr;
+    float *H = nullptr, *P = nullptr;  // residual stream; projection outputs / split-K partials
     void *Xn = nullptr, *Qb = nullptr, *Ob = nullptr, *Ab = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
-    float *skinny_part = nullptr;
-    size_t skinny_part_floats = 0;
-    int *counters = nullptr;
-    int n_counters = 0;
     float *attn_part = nullptr;
     size_t attn_part_floats = 0;
     char *d_tables = nullptr;
@@ -58,18 +54,33 @@ struct kvr_ctx {
     hipEvent_t stage_ev = nullptr;
     bool stage_pending = false;
 
+    // per-step event profiling
+    bool profiling = false;
+    std::vector<hipEvent_t> ev_pool;
+    std::vector<std::pair<int, hipEvent_t>> ev_marks;  // (step ending at this event, or -1), event
+    double step_ms[16] = {};
+    long long step_n[16] = {};
+
     std::string err;
 };
 
 namespace {
 
 constexpr int PREFILL_CHUNK = 8192;
-constexpr size_t SKINNY_PART_BYTES = 64ull << 20;
 constexpr size_t ATTN_PART_BYTES = 64ull << 20;
-constexpr int N_COUNTERS = 1 << 16;
 constexpr int PART_ROW = ATT_HD + 4;
+constexpr int SPLIT_MAX = 32;
+
+enum Step { ST_EMBED, ST_NORM, ST_QKV, ST_ROPE, ST_ATTN, ST_COMBINE, ST_OPROJ, ST_GATEUP, ST_DOWN, ST_FINAL, ST_COUNT };
+const char *const STEP_NAMES[ST_COUNT] = {"embed", "rmsnorm", "qkv_proj", "rope_scatter", "attention",
+                                          "attention_combine", "o_proj", "gate_up_swiglu", "down_proj", "final_norm"};
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int env_int(const char *name, int dflt) {
+    const char *v = getenv(name);
+    return (v && *v) ? atoi(v) : dflt;
+}
 
 kvr_status fail(kvr_ctx *c, kvr_status st, const std::string &msg) {
     if (c) c->err = msg;
@@ -109,24 +120,25 @@ struct Tables {
 void plan_attention(const kvr_ctx *c, Tables &t) {
     const int Hkv = c->d.n_kv_heads;
     const int G = c->d.n_heads / Hkv;
+    const int rows_blk = 16 * attention_row_tiles(c->d.n_heads, Hkv);
     struct Block { int doc, row0, nrows, kmax; };
     std::vector<Block> blocks;
     for (int di = 0; di < (int)t.docs.size(); ++di) {
         const DocInfo &dc = t.docs[di];
-        for (int b = 0; b < dc.nrows; b += ATT_ROWS) {
-            const int nb = std::min(ATT_ROWS, dc.nrows - b);
+        for (int b = 0; b < dc.nrows; b += rows_blk) {
+            const int nb = std::min(rows_blk, dc.nrows - b);
             blocks.push_back({di, dc.row0 + b, nb, t.rows[dc.row0 + b + nb - 1].pos + 1});
         }
     }
-    const int target = 1024;
+    const int target = env_int("KVR_ATT_TARGET", 768);
     long long total_keys = 0;
     for (auto &b : blocks) total_keys += b.kmax;
     int KS = 1 << 30;
-    const size_t slot_floats = (size_t)G * ATT_ROWS * PART_ROW;
+    const size_t slot_floats = (size_t)G * rows_blk * PART_ROW;
     const size_t max_slots = c->attn_part_floats / slot_floats;
     if ((long long)blocks.size() * Hkv < target / 2) {
         long long ks = (total_keys * Hkv + target - 1) / target;
-        ks = std::max<long long>(256, (ks + ATT_KT - 1) / ATT_KT * ATT_KT);
+        ks = std::max<long long>(env_int("KVR_ATT_MINKS", 128), (ks + ATT_KT - 1) / ATT_KT * ATT_KT);
         for (;; ks *= 2) {
             size_t slots = 0, nitems = 0;
             for (auto &b : blocks) {
@@ -159,45 +171,73 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
                      [](const AttnItem &x, const AttnItem &y) { return (x.k1 - x.k0) > (y.k1 - y.k0); });
 }
 
-// Split factor of the skinny linear layer: about 1024 blocks, each wavefront
-// keeping at least 8 k-steps of 32, and the partial tiles within the scratch.
-int skinny_split(const kvr_ctx *c, int tiles, int K, int R, int fw) {
-    const char *env = getenv("KVR_SKINNY_SPLIT");
-    const int ksteps = K / 32;
-    const int smax = std::max(1, ksteps / 32);
-    int s = env ? atoi(env) : std::max(1, (1024 + tiles - 1) / tiles);
-    s = std::max(1, std::min(s, smax));
-    while (s > 1 && (size_t)tiles * s * R * fw > c->skinny_part_floats) --s;
-    return s;
+// Weight tiles per wavefront and split-K factor of a skinny projection: about
+// 512 blocks, at least 8 k-steps of 32 per wavefront, never split for SwiGLU.
+struct SkinnyPlan { int nt, split; };
+
+SkinnyPlan plan_skinny(int ncols, int K, bool swiglu, const char *env_nt, const char *env_split) {
+    SkinnyPlan p;
+    p.nt = ncols % 64 == 0 ? 4 : (ncols % 32 == 0 ? 2 : 1);
+    const int nt = env_int(env_nt, 0);
+    if ((nt == 1 || nt == 2 || nt == 4) && ncols % (16 * nt) == 0) p.nt = nt;
+    if (swiglu && p.nt < 2) p.nt = 2;
+    const int tiles = ncols / (16 * p.nt);
+    if (swiglu) { p.split = 1; return p; }
+    const int smax = std::max(1, std::min(SPLIT_MAX, (K / 32) / 32));
+    p.split = std::max(1, std::min(smax, (512 + tiles - 1) / tiles));
+    const int es = env_int(env_split, 0);
+    if (es >= 1) p.split = std::min(es, std::min(SPLIT_MAX, K / 32));
+    return p;
+}
+
+bool skinny_pass_ok(const kvr_ctx *c, int R) {
+    const kvr_dims &d = c->d;
+    const int qd = d.n_heads * d.head_dim, kd = d.n_kv_heads * d.head_dim;
+    return c->bf16 && !c->force_simple && R <= 64 && d.d_model % 32 == 0 && qd % 32 == 0 && d.d_ffn % 32 == 0 &&
+           (qd + 2 * kd) % 16 == 0 && d.d_model % 16 == 0;
 }
 
 hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
     if (!c->bf16 || c->force_simple) return launch_linear_simple(c->bf16, epi, a, s);
-    const int ncols = epi == EPI_SWIGLU ? 2 * a.N : a.N;
-    const bool kok = a.K % 32 == 0 && a.ldx % 8 == 0;
-    if (a.R <= 64 && kok) {
-        const int nt = (ncols % 64 == 0) ? 4 : (ncols % 32 == 0 ? 2 : 0);
-        if (nt) {
-            const int fw = 16 * nt;
-            const int tiles = ncols / fw;
-            if (tiles <= c->n_counters)
-                return launch_linear_skinny(epi, a, skinny_split(c, tiles, a.K, a.R, fw), nt, s);
-        }
-    }
     if (a.K % 64 == 0 && a.ldx % 8 == 0 && (epi == EPI_SWIGLU ? a.N % 64 == 0 : a.N % 128 == 0))
         return launch_linear_tiled(epi, a, s);
     return launch_linear_simple(c->bf16, epi, a, s);
 }
 
 LinearArgs make_args(const void *x, int ldx, int R, int K, int N, const void *w0, const void *w1, const void *w2,
-                     int e0, int e1, void *out, int ldo, kvr_ctx *c) {
+                     int e0, int e1, void *out, int ldo) {
     LinearArgs a{};
     a.x = x; a.ldx = ldx; a.R = R; a.K = K; a.N = N;
     a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
     a.out = out; a.ldo = ldo;
-    a.partial = c->skinny_part; a.counters = c->counters;
     return a;
+}
+
+hipError_t skinny(int epi, const void *x, int R, int K, int N, const void *w0, const void *w1, const void *w2, int e0,
+                  int e1, void *out, const SkinnyPlan &p, hipStream_t s) {
+    SkinnyArgs a{};
+    a.x = x; a.R = R; a.K = K; a.N = N;
+    a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
+    a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
+    a.out = out; a.split = p.split;
+    return launch_linear_skinny(epi, a, p.nt, s);
+}
+
+// Profiling mark: the event ends the launch(es) of `step` enqueued since the
+// previous mark (-1 opens a pass).
+hipError_t mark(kvr_ctx *c, int step, hipStream_t s) {
+    if (!c->profiling) return hipSuccess;
+    hipEvent_t ev;
+    if (!c->ev_pool.empty()) {
+        ev = c->ev_pool.back();
+        c->ev_pool.pop_back();
+    } else {
+        hipError_t e = hipEventCreate(&ev);
+        if (e != hipSuccess) return e;
+    }
+    c->ev_marks.push_back({step, ev});
+    return hipEventRecord(ev, s);
 }
 
 // Upload the tables of a pass and enqueue its kernels.
@@ -205,7 +245,8 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     const kvr_dims &d = c->d;
     const int R = (int)t.rows.size();
     if (R == 0) return KVR_OK;
-    const bool attn_mfma = c->bf16 && !c->force_simple && d.head_dim == ATT_HD && d.n_heads / d.n_kv_heads <= 8;
+    const bool attn_mfma = c->bf16 && !c->force_simple && d.head_dim == ATT_HD && d.n_heads / d.n_kv_heads <= 16;
+    const bool sk = skinny_pass_ok(c, R);
     if (attn_mfma) plan_attention(c, t);
     if ((int)t.items.size() > c->items_cap || (int)t.comb.size() > c->comb_cap)
         return fail(c, KVR_E_RANGE, "attention plan exceeds the context's item capacity");
@@ -236,40 +277,76 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     const CombineItem *comb = (const CombineItem *)(c->d_tables + o_comb);
 
     const int D = d.d_model, F = d.d_ffn, hd = d.head_dim;
-    const int qd = d.n_heads * hd, kd = d.n_kv_heads * hd;
+    const int qd = d.n_heads * hd, kd = d.n_kv_heads * hd, NQKV = qd + 2 * kd;
     const bool bf = c->bf16;
-#define KVR_CHECK(expr, what)                          \
-    do {                                               \
-        hipError_t err_ = (expr);                      \
-        if (err_ != hipSuccess) return hip_fail(c, err_, what); \
+    SkinnyPlan p_qkv{}, p_o{}, p_gu{}, p_down{};
+    if (sk) {
+        p_qkv = plan_skinny(NQKV, D, false, "KVR_NT_QKV", "KVR_SPLIT_QKV");
+        p_o = plan_skinny(D, qd, false, "KVR_NT_O", "KVR_SPLIT_O");
+        p_gu = plan_skinny(2 * F, D, true, "KVR_NT_GATEUP", nullptr);
+        p_down = plan_skinny(D, F, false, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
+    }
+#define KVR_CHECK(expr, what, step)                                  \
+    do {                                                             \
+        hipError_t err_ = (expr);                                    \
+        if (err_ == hipSuccess) err_ = mark(c, step, s);             \
+        if (err_ != hipSuccess) return hip_fail(c, err_, what);      \
     } while (0)
 
-    KVR_CHECK(launch_embed(bf, rows, docs, R, c->embed, D, d.vocab, c->H, s), "embed");
+    KVR_CHECK(hipSuccess, "profiling mark", -1);
+    KVR_CHECK(launch_embed(bf, rows, docs, R, c->embed, D, d.vocab, c->H, s), "embed", ST_EMBED);
+    int resid_split = 0;  // partial tiles in P still to be added to H
     for (int l = 0; l < d.n_layers; ++l) {
         const kvr_layer_weights &w = c->layers[l];
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, w.attn_norm, R, D, d.rms_eps, c->Xn, D, s), "rmsnorm(attn)");
-        KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, D, R, D, qd + 2 * kd, w.wq, w.wk, w.wv, qd, qd + kd, c->QKV,
-                                                 qd + 2 * kd, c), s), "linear(qkv)");
-        KVR_CHECK(launch_rope_scatter(bf, c->QKV, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd,
-                                      c->rope_cos, c->rope_sin, c->Qb, s), "rope_scatter");
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, D, sk, s),
+                  "rmsnorm(attn)", ST_NORM);
+        int qkv_split = 1;
+        if (sk) {
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, p_qkv, s), "qkv",
+                      ST_QKV);
+            qkv_split = p_qkv.split;
+        } else {
+            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, NQKV), s),
+                      "qkv", ST_QKV);
+        }
+        KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
+                                      hd, c->rope_cos, c->rope_sin, c->Qb, s), "rope_scatter", ST_ROPE);
         if (attn_mfma) {
             KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, rows, docs, items, (int)t.items.size(), l,
-                                            d.n_heads, d.n_kv_heads, c->attn_part, (bf16_t *)c->Ob, s), "attention");
-            KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
-                                               (bf16_t *)c->Ob, s), "attention_combine");
+                                            d.n_heads, d.n_kv_heads, c->attn_part, (bf16_t *)c->Ob, sk, s),
+                      "attention", ST_ATTN);
+            if (!t.comb.empty())
+                KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
+                                                   (bf16_t *)c->Ob, sk, s), "attention_combine", ST_COMBINE);
         } else {
-            KVR_CHECK(launch_attention_simple(bf, c->Qb, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob, s),
-                      "attention_simple");
+            KVR_CHECK(launch_attention_simple(bf, c->Qb, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob, sk, s),
+                      "attention_simple", ST_ATTN);
         }
-        KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, D, c), s),
-                  "linear(o)");
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, w.mlp_norm, R, D, d.rms_eps, c->Xn, D, s), "rmsnorm(mlp)");
-        KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, F, c), s),
-                  "linear(gate_up)");
-        KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H, D, c), s),
-                  "linear(down)");
+        if (sk) {
+            KVR_CHECK(skinny(EPI_STORE, c->Ob, R, qd, D, w.wo, w.wo, w.wo, D, D, c->P, p_o, s), "o_proj", ST_OPROJ);
+            resid_split = p_o.split;
+        } else {
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, D), s),
+                      "o_proj", ST_OPROJ);
+        }
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, D, sk, s),
+                  "rmsnorm(mlp)", ST_NORM);
+        resid_split = 0;
+        if (sk) {
+            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, p_gu, s), "gate_up",
+                      ST_GATEUP);
+            KVR_CHECK(skinny(EPI_STORE, c->Ab, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->P, p_down, s), "down",
+                      ST_DOWN);
+            resid_split = p_down.split;
+        } else {
+            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, F), s),
+                      "gate_up", ST_GATEUP);
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H, D), s),
+                      "down", ST_DOWN);
+        }
     }
-    KVR_CHECK(launch_final_norm(bf, c->H, c->final_norm, rows, docs, R, D, d.rms_eps, s), "final_norm");
+    KVR_CHECK(launch_final_norm(bf, c->H, c->P, resid_split, c->final_norm, rows, docs, R, D, d.rms_eps, s),
+              "final_norm", ST_FINAL);
 #undef KVR_CHECK
     return KVR_OK;
 }
@@ -342,38 +419,34 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     c->max_docs = std::max(1, d.max_rows);
     const int G = d.n_heads / d.n_kv_heads;
     c->attn_part_floats = ATTN_PART_BYTES / 4;
-    const size_t slot_floats = (size_t)G * ATT_ROWS * PART_ROW;
+    const size_t slot_floats = (size_t)G * 16 * PART_ROW;
     const int max_slots = (int)(c->attn_part_floats / slot_floats);
-    const int blocks_cap = c->rows_cap / ATT_ROWS + c->max_docs + 1;
+    const int blocks_cap = c->rows_cap / 16 + c->max_docs + 1;
     c->items_cap = blocks_cap * d.n_kv_heads + max_slots;
     c->comb_cap = blocks_cap * d.n_kv_heads;
-    c->skinny_part_floats = SKINNY_PART_BYTES / 4;
-    c->n_counters = N_COUNTERS;
     c->tables_bytes = align_up((size_t)c->rows_cap * sizeof(RowInfo), 256) +
                       align_up((size_t)c->max_docs * sizeof(DocInfo), 256) +
                       align_up((size_t)c->items_cap * sizeof(AttnItem), 256) + (size_t)c->comb_cap * sizeof(CombineItem);
 
-    const size_t R = (size_t)c->rows_cap;
+    const size_t R = align_up((size_t)c->rows_cap, 64);
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
-    const size_t o_H = take(R * D * 4), o_QKV = take(R * (qd + 2 * kd) * 4), o_Xn = take(R * D * es),
+    const size_t p_floats = std::max(R * (qd + 2 * kd), (size_t)SPLIT_MAX * 64 * std::max(qd + 2 * kd, D));
+    const size_t o_H = take(R * D * 4), o_P = take(p_floats * 4), o_Xn = take(R * D * es),
                  o_Qb = take(R * qd * es), o_Ob = take(R * qd * es), o_Ab = take(R * F * es),
                  o_cos = take((size_t)d.max_ctx * (hd / 2) * 4), o_sin = take((size_t)d.max_ctx * (hd / 2) * 4),
-                 o_sp = take(c->skinny_part_floats * 4), o_cnt = take((size_t)c->n_counters * 4),
                  o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes);
     c->ws_bytes = off;
     e = hipMalloc((void **)&c->ws, c->ws_bytes);
     if (e != hipSuccess) { delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: workspace allocation failed"); }
     c->H = (float *)(c->ws + o_H);
-    c->QKV = (float *)(c->ws + o_QKV);
+    c->P = (float *)(c->ws + o_P);
     c->Xn = c->ws + o_Xn;
     c->Qb = c->ws + o_Qb;
     c->Ob = c->ws + o_Ob;
     c->Ab = c->ws + o_Ab;
     c->rope_cos = (float *)(c->ws + o_cos);
     c->rope_sin = (float *)(c->ws + o_sin);
-    c->skinny_part = (float *)(c->ws + o_sp);
-    c->counters = (int *)(c->ws + o_cnt);
     c->attn_part = (float *)(c->ws + o_ap);
     c->d_tables = c->ws + o_tab;
 
@@ -396,7 +469,6 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
             }
         e = hipMemcpy(c->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice);
         if (e == hipSuccess) e = hipMemcpy(c->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice);
-        if (e == hipSuccess) e = hipMemset(c->counters, 0, (size_t)c->n_counters * 4);
         if (e != hipSuccess) {
             (void)hipEventDestroy(c->stage_ev); (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c;
             return hip_fail(nullptr, e, "kvr_create: workspace initialisation");
@@ -412,6 +484,8 @@ void kvr_destroy(kvr_ctx *c) {
         DeviceGuard g(c->device);
         (void)hipDeviceSynchronize();
         if (c->stage_ev) (void)hipEventDestroy(c->stage_ev);
+        for (auto &m : c->ev_marks) (void)hipEventDestroy(m.second);
+        for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
         if (c->h_stage) (void)hipHostFree(c->h_stage);
         if (c->ws) (void)hipFree(c->ws);
     }
@@ -440,24 +514,39 @@ kvr_status kvr_prefill(kvr_ctx *c, const int32_t *d_tokens, int32_t n, int32_t n
     return KVR_OK;
 }
 
-kvr_status kvr_linear(kvr_ctx *c, kvr_epilogue epi, const void *d_x, int32_t rows, int32_t in_features,
-                      const void *d_w, const void *d_w2, int32_t out_features, void *d_out, void *stream) {
-    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_linear: NULL context");
-    if (epi != KVR_EPI_STORE && epi != KVR_EPI_ADD && epi != KVR_EPI_SWIGLU)
-        return fail(c, KVR_E_ARG, "kvr_linear: unknown epilogue");
-    if (!d_x || !d_w || !d_out || (epi == KVR_EPI_SWIGLU) != (d_w2 != nullptr))
-        return fail(c, KVR_E_ARG, "kvr_linear: NULL pointer (d_w2 is required for SWIGLU only)");
-    if (!aligned16(d_x) || !aligned16(d_w) || !aligned16(d_out) || (d_w2 && !aligned16(d_w2)))
-        return fail(c, KVR_E_ARG, "kvr_linear: pointers must be 16-byte aligned");
-    if (rows < 1 || rows > c->rows_cap || in_features < 1 || out_features < 1)
-        return fail(c, KVR_E_RANGE, "kvr_linear: rows must be in [1, row capacity] and features positive");
+kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_profile_enable: NULL context");
+    c->profiling = enable != 0;
+    return KVR_OK;
+}
+
+kvr_status kvr_profile_read(kvr_ctx *c, int32_t capacity, const char **names, double *total_ms, int64_t *launches,
+                            int32_t *n_steps) {
+    if (!c || !n_steps || capacity < 0 || (capacity > 0 && (!names || !total_ms || !launches)))
+        return fail(c, KVR_E_ARG, "kvr_profile_read: bad arguments");
     DeviceGuard g(c->device);
-    const int e = epi == KVR_EPI_STORE ? EPI_STORE : (epi == KVR_EPI_ADD ? EPI_RESID : EPI_SWIGLU);
-    const void *w1 = d_w2 ? d_w2 : d_w;
-    LinearArgs a = make_args(d_x, in_features, rows, in_features, out_features, d_w, w1, w1, out_features,
-                             out_features, d_out, out_features, c);
-    hipError_t err = linear(c, e, a, (hipStream_t)stream);
-    if (err != hipSuccess) return hip_fail(c, err, "kvr_linear");
+    if (!c->ev_marks.empty()) {
+        hipError_t e = hipEventSynchronize(c->ev_marks.back().second);
+        if (e != hipSuccess) return hip_fail(c, e, "kvr_profile_read");
+        for (size_t i = 1; i < c->ev_marks.size(); ++i) {
+            const int st = c->ev_marks[i].first;
+            if (st < 0) continue;
+            float ms = 0.f;
+            e = hipEventElapsedTime(&ms, c->ev_marks[i - 1].second, c->ev_marks[i].second);
+            if (e != hipSuccess) return hip_fail(c, e, "kvr_profile_read: hipEventElapsedTime");
+            c->step_ms[st] += ms;
+            c->step_n[st] += 1;
+        }
+        for (auto &m : c->ev_marks) c->ev_pool.push_back(m.second);
+        c->ev_marks.clear();
+    }
+    *n_steps = ST_COUNT;
+    for (int i = 0; i < ST_COUNT && i < capacity; ++i) {
+        names[i] = STEP_NAMES[i];
+        total_ms[i] = c->step_ms[i];
+        launches[i] = c->step_n[i];
+    }
+    for (int i = 0; i < ST_COUNT; ++i) { c->step_ms[i] = 0.0; c->step_n[i] = 0; }
     return KVR_OK;
 }
 

@@ -51,11 +51,11 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
         bg[i] = base + (size_t)row * K + lk;
     }
 
-    uint4 ra[4], rb[4];
+    u32x4 ra[4], rb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        ra[i] = *reinterpret_cast<const uint4 *>(ag[i]);
-        rb[i] = *reinterpret_cast<const uint4 *>(bg[i]);
+        ra[i] = *reinterpret_cast<const u32x4 *>(ag[i]);
+        rb[i] = *reinterpret_cast<const u32x4 *>(bg[i]);
     }
 
     f32x4 acc[4][4];
@@ -69,15 +69,15 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            *reinterpret_cast<uint4 *>(&As[(lrow + 32 * i) * LDS_STRIDE + lk]) = ra[i];
-            *reinterpret_cast<uint4 *>(&Bs[(lrow + 32 * i) * LDS_STRIDE + lk]) = rb[i];
+            *reinterpret_cast<u32x4 *>(&As[(lrow + 32 * i) * LDS_STRIDE + lk]) = ra[i];
+            *reinterpret_cast<u32x4 *>(&Bs[(lrow + 32 * i) * LDS_STRIDE + lk]) = rb[i];
         }
         __syncthreads();
         if (k0 + BK < K) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                ra[i] = *reinterpret_cast<const uint4 *>(ag[i] + k0 + BK);
-                rb[i] = *reinterpret_cast<const uint4 *>(bg[i] + k0 + BK);
+                ra[i] = *reinterpret_cast<const u32x4 *>(ag[i] + k0 + BK);
+                rb[i] = *reinterpret_cast<const u32x4 *>(bg[i] + k0 + BK);
             }
         }
 #pragma unroll

@@ -37,58 +37,132 @@ __global__ __launch_bounds__(256) void embed_kernel(const RowInfo *rows, const D
     for (int i = threadIdx.x; i < d; i += 256) H[(size_t)r * d + i] = to_f32(src[i]);
 }
 
-// X = H * rsqrt(mean(H^2) + eps) * gain, written in the operand type.
-template <typename TO, typename TG>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float *H, const TG *gain, int d, float eps, TO *X,
-                                                      int ldx) {
-    __shared__ float red[4];
+// Sum over a 1024-thread block.
+__device__ __forceinline__ float block_sum1024(float v, float *red) {
+    v = warp_sum(v);
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    if (l == 0) red[w] = v;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) t += red[q];
+    __syncthreads();
+    return t;
+}
+
+// h4 = H[r][4i..4i+3] + the split-K partial tiles part[q][r][4i..] in order.
+__device__ __forceinline__ float4 add_partials(float4 h, const float *part, int nsplit, int R, int r, int d, int i) {
+    int q = 0;
+    for (; q + 4 <= nsplit; q += 4) {
+        float4 p[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) p[u] = *reinterpret_cast<const float4 *>(part + ((size_t)(q + u) * R + r) * d + 4 * i);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) { h.x += p[u].x; h.y += p[u].y; h.z += p[u].z; h.w += p[u].w; }
+    }
+    for (; q < nsplit; ++q) {
+        const float4 p = *reinterpret_cast<const float4 *>(part + ((size_t)q * R + r) * d + 4 * i);
+        h.x += p.x; h.y += p.y; h.z += p.z; h.w += p.w;
+    }
+    return h;
+}
+
+// H[r] += sum of the split-K partial tiles (fixed order), then
+// X = H * rsqrt(mean(H^2) + eps) * gain in the operand type (row-major or
+// operand order).  One 1024-thread block per row, four columns per thread
+// per pass (d % 4 == 0).
+template <typename TO, typename TG, bool PERM>
+__global__ __launch_bounds__(1024) void rmsnorm_kernel(float *H, const float *part, int nsplit, int R,
+                                                       const TG *gain, int d, float eps, TO *X, int ldx) {
+    __shared__ float red[16];
     const int r = blockIdx.x;
-    const float *h = H + (size_t)r * d;
+    float *h = H + (size_t)r * d;
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss += h[i] * h[i];
-    ss = block_sum256(ss, red);
+    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
+        float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
+        if (nsplit) {
+            v = add_partials(v, part, nsplit, R, r, d, i);
+            *reinterpret_cast<float4 *>(h + 4 * i) = v;
+        }
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = block_sum1024(ss, red);
     const float inv = rsqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; i < d; i += 256) X[(size_t)r * ldx + i] = from_f32<TO>(h[i] * inv * to_f32(gain[i]));
+    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
+        const float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int c = 4 * i + e;
+            const TO y = from_f32<TO>(vv[e] * inv * to_f32(gain[c]));
+            if (PERM) X[perm_offset(r, c, d)] = y;
+            else X[(size_t)r * ldx + c] = y;
+        }
+    }
 }
 
 template <typename TG>
-__global__ __launch_bounds__(256) void final_norm_kernel(const float *H, const TG *gain, const RowInfo *rows,
-                                                         const DocInfo *docs, int d, float eps) {
-    __shared__ float red[4];
+__global__ __launch_bounds__(1024) void final_norm_kernel(float *H, const float *part, int nsplit, int R,
+                                                          const TG *gain, const RowInfo *rows, const DocInfo *docs,
+                                                          int d, float eps) {
+    __shared__ float red[16];
     const int r = blockIdx.x;
     const RowInfo ri = rows[r];
     float *dst = docs[ri.doc].hidden_out;
+    float *h = H + (size_t)r * d;
+    float ss = 0.f;
+    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
+        float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
+        if (nsplit) {
+            v = add_partials(v, part, nsplit, R, r, d, i);
+            *reinterpret_cast<float4 *>(h + 4 * i) = v;
+        }
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = block_sum1024(ss, red);
     if (!dst) return;
     dst += (size_t)ri.out * d;
-    const float *h = H + (size_t)r * d;
-    float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss += h[i] * h[i];
-    ss = block_sum256(ss, red);
     const float inv = rsqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; i < d; i += 256) dst[i] = h[i] * inv * to_f32(gain[i]);
+    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
+        const float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
+        float4 o;
+        o.x = v.x * inv * to_f32(gain[4 * i]);
+        o.y = v.y * inv * to_f32(gain[4 * i + 1]);
+        o.z = v.z * inv * to_f32(gain[4 * i + 2]);
+        o.w = v.w * inv * to_f32(gain[4 * i + 3]);
+        *reinterpret_cast<float4 *>(dst + 4 * i) = o;
+    }
 }
 
 // Adds the Q/K/V bias, rotates Q and K at the row's absolute position
 // (rotate-half pairing) and scatters K and V into the row's cache slot; Q goes
 // to the attention operand buffer [R][Hq*hd].
 template <typename T>
-__global__ __launch_bounds__(256) void rope_scatter_kernel(const float *qkv, const T *bq, const T *bk, const T *bv,
-                                                           const RowInfo *rows, const DocInfo *docs, int layer,
-                                                           int Hq, int Hkv, int hd, const float *rcos,
-                                                           const float *rsin, T *Q) {
+__global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, int nsplit, int R, const T *bq,
+                                                           const T *bk, const T *bv, const RowInfo *rows,
+                                                           const DocInfo *docs, int layer, int Hq, int Hkv, int hd,
+                                                           const float *rcos, const float *rsin, T *Q) {
     const int r = blockIdx.x;
     const RowInfo ri = rows[r];
     const DocInfo dc = docs[ri.doc];
     const int half = hd >> 1;
     const int qd = Hq * hd, kd = Hkv * hd;
-    const float *row = qkv + (size_t)r * (qd + 2 * kd);
+    const int N = qd + 2 * kd;
+    // sum the split-K partial tiles of this row into LDS first
+    extern __shared__ float row[];
+    for (int i = threadIdx.x; 4 * i < N; i += 1024) {
+        float4 v = *reinterpret_cast<const float4 *>(qkv + (size_t)r * N + 4 * i);
+        if (nsplit > 1) v = add_partials(v, qkv + (size_t)R * N, nsplit - 1, R, r, N, i);
+        *reinterpret_cast<float4 *>(row + 4 * i) = v;
+    }
+    __syncthreads();
     const float *cs = rcos + (size_t)ri.pos * half;
     const float *sn = rsin + (size_t)ri.pos * half;
     T *cache = (T *)dc.cache;
     const size_t head_stride = (size_t)dc.n_cap * hd;
     T *kbase = cache + ((size_t)layer * 2 + 0) * Hkv * head_stride + (size_t)ri.pos * hd;
     T *vbase = cache + ((size_t)layer * 2 + 1) * Hkv * head_stride + (size_t)ri.pos * hd;
-    for (int idx = threadIdx.x; idx < (Hq + Hkv) * half; idx += 256) {
+    for (int idx = threadIdx.x; idx < (Hq + Hkv) * half; idx += 1024) {
         const int j = idx / half, i = idx - j * half;
         float a, b;
         if (j < Hq) {
@@ -112,7 +186,7 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *qkv, con
             kbase[g * head_stride + i + half] = from_f32<T>(o2);
         }
     }
-    for (int idx = threadIdx.x; idx < kd; idx += 256) {
+    for (int idx = threadIdx.x; idx < kd; idx += 1024) {
         const int g = idx / hd, i = idx - g * hd;
         float v = row[qd + kd + idx];
         if (bv) v += to_f32(bv[idx]);
@@ -123,7 +197,7 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float *qkv, con
 // One wavefront per (row, query head): online softmax over keys 0..pos.
 template <typename T>
 __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const RowInfo *rows, const DocInfo *docs,
-                                                              int layer, int Hq, int Hkv, int hd, T *O) {
+                                                              int layer, int Hq, int Hkv, int hd, T *O, int o_perm) {
     const int r = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
     const RowInfo ri = rows[r];
     const DocInfo dc = docs[ri.doc];
@@ -151,8 +225,9 @@ __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const 
         m = mn;
     }
     const float inv = 1.0f / l;
-    if (has0) O[(size_t)r * qd + j * hd + lane] = from_f32<T>(a0 * inv);
-    if (has1) O[(size_t)r * qd + j * hd + lane + 64] = from_f32<T>(a1 * inv);
+    if (has0) O[o_perm ? perm_offset(r, j * hd + lane, qd) : (size_t)r * qd + j * hd + lane] = from_f32<T>(a0 * inv);
+    if (has1)
+        O[o_perm ? perm_offset(r, j * hd + lane + 64, qd) : (size_t)r * qd + j * hd + lane + 64] = from_f32<T>(a1 * inv);
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
@@ -250,60 +325,68 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
     return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, const float *H, const void *gain, int R, int d, float eps,
-                          void *X, int ldx, hipStream_t s) {
+hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
+                          int R, int d, float eps, void *X, int ldx, bool perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
-    if (bf16_out && bf16_gain)
-        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t>), dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, d, eps,
-                           (bf16_t *)X, ldx);
-    else if (!bf16_out && !bf16_gain)
-        hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(R), dim3(256), 0, s, H, (const float *)gain, d, eps,
-                           (float *)X, ldx);
-    else if (bf16_out)
-        hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, float>), dim3(R), dim3(256), 0, s, H, (const float *)gain, d, eps,
-                           (bf16_t *)X, ldx);
-    else
-        hipLaunchKernelGGL((rmsnorm_kernel<float, bf16_t>), dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, d, eps,
-                           (float *)X, ldx);
+    if (d % 4 != 0) return hipErrorInvalidValue;
+    if (bf16_out && bf16_gain) {
+        if (perm)
+            hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, true>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+                               (const bf16_t *)gain, d, eps, (bf16_t *)X, ldx);
+        else
+            hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+                               (const bf16_t *)gain, d, eps, (bf16_t *)X, ldx);
+    } else if (!bf16_out && !bf16_gain && !perm) {
+        hipLaunchKernelGGL((rmsnorm_kernel<float, float, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+                           (const float *)gain, d, eps, (float *)X, ldx);
+    } else {
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_final_norm(bool bf16_gain, const float *H, const void *gain, const RowInfo *rows,
-                             const DocInfo *docs, int R, int d, float eps, hipStream_t s) {
+hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
+                             const RowInfo *rows, const DocInfo *docs, int R, int d, float eps, hipStream_t s) {
     if (R <= 0) return hipSuccess;
+    if (d % 4 != 0) return hipErrorInvalidValue;
     if (bf16_gain)
-        hipLaunchKernelGGL(final_norm_kernel<bf16_t>, dim3(R), dim3(256), 0, s, H, (const bf16_t *)gain, rows, docs,
-                           d, eps);
+        hipLaunchKernelGGL(final_norm_kernel<bf16_t>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+                           (const bf16_t *)gain, rows, docs, d, eps);
     else
-        hipLaunchKernelGGL(final_norm_kernel<float>, dim3(R), dim3(256), 0, s, H, (const float *)gain, rows, docs, d,
-                           eps);
+        hipLaunchKernelGGL(final_norm_kernel<float>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+                           (const float *)gain, rows, docs, d, eps);
     return hipGetLastError();
 }
 
-hipError_t launch_rope_scatter(bool bf16, const float *qkv, const void *bq, const void *bk, const void *bv,
-                               const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd,
-                               const float *rope_cos, const float *rope_sin, void *Q, hipStream_t s) {
+hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const void *bq, const void *bk,
+                               const void *bv, const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq,
+                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q,
+                               hipStream_t s) {
     if (R <= 0) return hipSuccess;
+    const size_t lds = (size_t)(Hq + 2 * Hkv) * hd * sizeof(float);
+    if (lds > 160 * 1024 || ((Hq + 2 * Hkv) * hd) % 4 != 0) return hipErrorInvalidValue;
     if (bf16)
-        hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, dim3(R), dim3(256), 0, s, qkv, (const bf16_t *)bq,
-                           (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
-                           (bf16_t *)Q);
+        hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
+                           (const bf16_t *)bq, (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd,
+                           rope_cos, rope_sin, (bf16_t *)Q);
     else
-        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(256), 0, s, qkv, (const float *)bq,
-                           (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
-                           (float *)Q);
+        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
+                           (const float *)bq, (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd,
+                           rope_cos, rope_sin, (float *)Q);
     return hipGetLastError();
 }
 
 hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
-                                   int layer, int Hq, int Hkv, int hd, void *O, hipStream_t s) {
+                                   int layer, int Hq, int Hkv, int hd, void *O, bool o_perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (bf16)
         hipLaunchKernelGGL(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q, rows, docs,
-                           layer, Hq, Hkv, hd, (bf16_t *)O);
-    else
+                           layer, Hq, Hkv, hd, (bf16_t *)O, (int)o_perm);
+    else if (!o_perm)
         hipLaunchKernelGGL(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q, rows, docs,
-                           layer, Hq, Hkv, hd, (float *)O);
+                           layer, Hq, Hkv, hd, (float *)O, 0);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
