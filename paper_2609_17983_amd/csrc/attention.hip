@@ -7,20 +7,22 @@
 // round-robin to the eight wavefronts of the block (two per SIMD); every
 // 64-key K/V tile staged in LDS serves all of them, so the cache is read once
 // per item.  Scores are computed transposed, S^T = K Q^T
-// (v_mfma_f32_16x16x32_bf16 with the key tile as A operand), so that each lane
+// (v_mfma_f32_16x16x32_bf16 with the key tile as A operand; Q is a compensated
+// bf16 pair hi + lo, so two MFMAs per k-step), so that each lane
 // owns one query row: the row max and sum of a tile are 16 in-lane values plus
 // two cross-lane steps.  The probabilities go straight from the S^T
-// accumulator into the B operand of O^T += V^T P^T: both operands enumerate the
+// accumulator into the B operand of O^T += V^T P^T (as a compensated pair, two
+// MFMAs per k-step): both operands enumerate the
 // 32 keys of a k-step in the same permuted order (slot j of lane group g <->
 // key 16*(j/4) + 4*g + j%4), so P never leaves registers; V is stored
 // transposed in LDS.  Softmax runs in the exp2 domain; the running max is only
 // raised (and the accumulators rescaled) when a row's tile max exceeds it by
 // more than 2^8, which keeps every probability below 256.  The causal mask is
 // applied only on tiles that reach a row's own position.  The next K/V tile is
-// fetched into registers while the current one is used.  When the key range of
-// a row block is split over several items (few rows, long contexts) each item
-// writes (m, l, unnormalised O) partials and a combine pass merges them with
-// log-sum-exp rescaling.
+// fetched into registers while the current one is used.  The output is written
+// as a compensated pair.  When the key range of a row block is split over
+// several items (few rows, long contexts) each item writes (m, l, unnormalised
+// O) partials and a combine pass merges them with log-sum-exp rescaling.
 #include <math.h>
 
 #include <algorithm>
@@ -57,10 +59,11 @@ __device__ __forceinline__ float xsum4(float v) {
 
 // PPW: (head, row tile) pairs per wavefront; MT: row tiles of a full item.
 template <int PPW>
-__global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t *Q, const RowInfo *rows,
-                                                                    const DocInfo *docs, const AttnItem *items,
-                                                                    int layer, int Hq, int Hkv, int MT, float *part,
-                                                                    bf16_t *O, int o_perm) {
+__global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t *Q, const bf16_t *Q_lo,
+                                                                    const RowInfo *rows, const DocInfo *docs,
+                                                                    const AttnItem *items, int layer, int Hq, int Hkv,
+                                                                    int MT, float *part, bf16_t *O, bf16_t *O_lo,
+                                                                    int o_perm) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS_STRIDE];
     __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * VT_STRIDE];
 
@@ -79,7 +82,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     // this wavefront's pairs: p = w + WAVES*i -> head t = p / MTi, row tile p % MTi
     bool pvalid[PPW];
     int pt[PPW], pm[PPW], prow[PPW];
-    bf16x8 qv[PPW][4];
+    bf16x8 qv[PPW][4], ql[PPW][4];
     f32x4 oacc[PPW][8];
     float m[PPW], l[PPW];
 #pragma unroll
@@ -93,7 +96,10 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         const int qrow = it.row0 + min(r, it.nrows - 1);
         const int j = it.kvh * G + pt[i];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) qv[i][ks] = ld16(Q + (size_t)qrow * qd + j * HD + ks * 32 + 8 * g);
+        for (int ks = 0; ks < 4; ++ks) {
+            qv[i][ks] = ld16(Q + (size_t)qrow * qd + j * HD + ks * 32 + 8 * g);
+            ql[i][ks] = ld16(Q_lo + (size_t)qrow * qd + j * HD + ks * 32 + 8 * g);
+        }
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) oacc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         m[i] = -INFINITY;
@@ -144,12 +150,14 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
                 if (!pvalid[i]) continue;
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks)
+                for (int ks = 0; ks < 4; ++ks) {
                     s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks], qv[i][ks], s[i][nt], 0, 0, 0);
+                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks], ql[i][ks], s[i][nt], 0, 0, 0);
+                }
             }
         }
         // online softmax, one query row per lane column
-        bf16x8 pb[PPW][2];
+        bf16x8 pb[PPW][2], pl[PPW][2];
 #pragma unroll
         for (int i = 0; i < PPW; ++i) {
             if (!pvalid[i]) continue;
@@ -193,13 +201,16 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
             // B operand P^T for 32-key step ks: slot j <-> key 32*ks + 16*(j/4) + 4*g + j%4
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                u32x4 u;
+                u32x4 u, v;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const f32x2 f = {s[i][2 * ks + q / 2][2 * (q % 2)], s[i][2 * ks + q / 2][2 * (q % 2) + 1]};
-                    u[q] = __builtin_bit_cast(unsigned int, __builtin_convertvector(f, bf16x2));
+                    const bf16x2 h = __builtin_convertvector(f, bf16x2);
+                    u[q] = __builtin_bit_cast(unsigned int, h);
+                    v[q] = __builtin_bit_cast(unsigned int, __builtin_convertvector(f - __builtin_convertvector(h, f32x2), bf16x2));
                 }
                 pb[i][ks] = __builtin_bit_cast(bf16x8, u);
+                pl[i][ks] = __builtin_bit_cast(bf16x8, v);
             }
         }
         // O^T += V^T P^T: A operand = V^T rows (dims 16*nt + lane%16) over the same key slots
@@ -218,8 +229,10 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
             for (int i = 0; i < PPW; ++i) {
                 if (!pvalid[i]) continue;
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
+                for (int ks = 0; ks < 2; ++ks) {
                     oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks], pb[i][ks], oacc[i][nt], 0, 0, 0);
+                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks], pl[i][ks], oacc[i][nt], 0, 0, 0);
+                }
             }
         }
     }
@@ -240,11 +253,18 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) {
                 const int c = j * HD + nt * 16 + 4 * g;  // 4 consecutive columns, 8-byte aligned
-                const f32x2 a = {oacc[i][nt][0] * inv, oacc[i][nt][1] * inv};
-                const f32x2 b = {oacc[i][nt][2] * inv, oacc[i][nt][3] * inv};
-                const uint2 v = make_uint2(__builtin_bit_cast(unsigned int, __builtin_convertvector(a, bf16x2)),
-                                           __builtin_bit_cast(unsigned int, __builtin_convertvector(b, bf16x2)));
-                *reinterpret_cast<uint2 *>(O + (o_perm ? perm_offset(r, c, qd) : (size_t)r * qd + c)) = v;
+                const size_t off = o_perm ? perm_offset(r, c, qd) : (size_t)r * qd + c;
+                uint32_t hi[2], lo[2];
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const f32x2 x = {oacc[i][nt][2 * q] * inv, oacc[i][nt][2 * q + 1] * inv};
+                    const bf16x2 h = __builtin_convertvector(x, bf16x2);
+                    const f32x2 back = __builtin_convertvector(h, f32x2);
+                    hi[q] = __builtin_bit_cast(unsigned int, h);
+                    lo[q] = __builtin_bit_cast(unsigned int, __builtin_convertvector(x - back, bf16x2));
+                }
+                *reinterpret_cast<uint2 *>(O + off) = make_uint2(hi[0], hi[1]);
+                *reinterpret_cast<uint2 *>(O_lo + off) = make_uint2(lo[0], lo[1]);
             }
         } else {
             float *p = part + ((size_t)(it.part * G + t) * rows_item + ri) * PART_ROW;
@@ -258,7 +278,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
 // One block per (combine item, query head of the group, row): merge the split
 // partials of one row in a single pass with running max rescaling (exp2 domain).
 __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
-                                                                int Hkv, int MT, bf16_t *O, int o_perm) {
+                                                                int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm) {
     const CombineItem it = items[blockIdx.x];
     const int t = blockIdx.y, i = blockIdx.z;
     if (i >= it.nrows) return;
@@ -278,7 +298,7 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
         M = Mn;
     }
     const int r = it.row0 + i, c = j * HD + d;
-    O[o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c] = f32_to_bf16(acc / L);
+    store_operand(O, O_lo, o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c, acc / L);
 }
 
 }  // namespace
@@ -288,29 +308,30 @@ int attention_row_tiles(int Hq, int Hkv) {
     return G >= 16 ? 1 : std::min(4, std::max(1, 16 / G));
 }
 
-hipError_t launch_attention_mfma(const bf16_t *Q, const RowInfo *rows, const DocInfo *docs, const AttnItem *items,
-                                 int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O, bool o_perm,
-                                 hipStream_t s) {
+hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
+                                 const AttnItem *items, int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O,
+                                 bf16_t *O_lo, bool o_perm, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
+    if (!Q_lo || !O_lo) return hipErrorInvalidValue;
     const int MT = attention_row_tiles(Hq, Hkv);
     const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
     if (ppw == 1)
-        hipLaunchKernelGGL(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, rows, docs, items, layer,
-                           Hq, Hkv, MT, part, O, (int)o_perm);
+        hipLaunchKernelGGL(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
     else if (ppw == 2)
-        hipLaunchKernelGGL(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, rows, docs, items, layer,
-                           Hq, Hkv, MT, part, O, (int)o_perm);
+        hipLaunchKernelGGL(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq, int Hkv,
-                                    bf16_t *O, bool o_perm, hipStream_t s) {
+                                    bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     const int MT = attention_row_tiles(Hq, Hkv);
     hipLaunchKernelGGL(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
-                       Hkv, MT, O, (int)o_perm);
+                       Hkv, MT, O, O_lo, (int)o_perm);
     return hipGetLastError();
 }
 

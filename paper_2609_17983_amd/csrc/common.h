@@ -38,6 +38,25 @@ template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
+// Matrix operands of the bf16 path are compensated pairs: x = hi + lo with
+// hi = bf16(x) and lo = bf16(x - hi), which carries x to about 16 significant
+// bits; a product with an exact bf16 weight is then two MFMAs into one fp32
+// accumulator.  For fp32 operands there is no low part (lo == nullptr).
+template <typename T>
+__device__ __forceinline__ void store_operand(T *hi, T *lo, size_t i, float x) {
+    if constexpr (sizeof(T) == 4) {
+        hi[i] = x;
+    } else {
+        const bf16_t h = f32_to_bf16(x);
+        hi[i] = h;
+        if (lo) lo[i] = f32_to_bf16(x - bf16_to_f32(h));
+    }
+}
+template <typename T>
+__device__ __forceinline__ float load_operand(const T *hi, const T *lo, size_t i) {
+    return lo ? to_f32(hi[i]) + to_f32(lo[i]) : to_f32(hi[i]);
+}
+
 // One repaired (or prefilled) row: its document, absolute position, and the row
 // index of its final hidden state inside the document's output buffer.
 struct RowInfo {
@@ -84,12 +103,14 @@ enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 // (gate, up) with output A[r][f] = silu(gate) * up.
 struct LinearArgs {
     const void *x;        // [R][K] operand (bf16 or fp32), row stride ldx
+    const void *x_lo;     // low part of a compensated bf16 operand, or null
     int32_t ldx;
     int32_t R, K, N;      // N: output columns (SWIGLU: number of features f)
     const void *w[3];     // row blocks of W
     int32_t seg_end[3];   // cumulative output-column boundaries of the blocks
     void *out;            // STORE: float [R][ldo]; RESID: float [R][ldo] (+=);
                           // SWIGLU: operand type [R][ldo]
+    void *out_lo;         // SWIGLU: low part of the compensated output, or null
     int32_t ldo;
     float *partial;       // split-K scratch
     int32_t *counters;    // split-K tile counters (kept at zero between calls)
@@ -98,11 +119,11 @@ struct LinearArgs {
 // Skinny (R <= 64) linear layer: X in operand order; STORE writes fp32 partial
 // tiles [split][R][N]; SWIGLU (split 1) writes silu(gate)*up in operand order.
 struct SkinnyArgs {
-    const void *x;
+    const void *x, *x_lo;  // compensated operand (hi, lo), both in operand order
     int32_t R, K, N;      // N: output columns (SWIGLU: number of features)
     const void *w[3];
     int32_t seg_end[3];
-    void *out;
+    void *out, *out_lo;    // SWIGLU writes a compensated pair
     int32_t split;
 };
 
@@ -115,25 +136,26 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
 // residual update; nsplit 0 = none), then X = H * rsqrt(mean(H^2)+eps) * gain,
 // row-major with stride ldx, or in operand order when `perm`.
 hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
-                          int R, int d, float eps, void *X, int ldx, bool perm, hipStream_t s);
+                          int R, int d, float eps, void *X, void *X_lo, int ldx, bool perm, hipStream_t s);
 hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
                              const RowInfo *rows, const DocInfo *docs, int R, int d, float eps, hipStream_t s);
 // qkv: `nsplit` fp32 tiles [nsplit][R][qd+2kd] summed in order.
 hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const void *bq, const void *bk,
                                const void *bv, const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq,
-                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q,
+                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q, void *Q_lo,
                                hipStream_t s);
 // O is written row-major [R][Hq*hd], or in operand order when o_perm.
-hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
-                                   int layer, int Hq, int Hkv, int hd, void *O, bool o_perm, hipStream_t s);
+hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, const RowInfo *rows,
+                                   const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd, void *O, void *O_lo,
+                                   bool o_perm, hipStream_t s);
 // 16-row tiles per attention work item for a head grouping (items carry up to
 // 16 * this many rows).
 int attention_row_tiles(int Hq, int Hkv);
-hipError_t launch_attention_mfma(const bf16_t *Q, const RowInfo *rows, const DocInfo *docs,
+hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
-                                 float *part, bf16_t *O, bool o_perm, hipStream_t s);
+                                 float *part, bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s);
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
-                                    int Hkv, bf16_t *O, bool o_perm, hipStream_t s);
+                                    int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s);
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
 // Skinny MFMA path (R <= 64); nt = 16-row weight tiles per wave (1, 2 or 4).
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s);

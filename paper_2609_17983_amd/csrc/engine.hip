@@ -43,7 +43,9 @@ struct kvr_ctx {
     char *ws = nullptr;
     size_t ws_bytes = 0;
     float *H = nullptr, *P = nullptr;  // residual stream; projection outputs / split-K partials
+    // matrix operands; in bf16 each is a compensated pair (hi, lo)
     void *Xn = nullptr, *Qb = nullptr, *Ob = nullptr, *Ab = nullptr;
+    void *Xn_lo = nullptr, *Qb_lo = nullptr, *Ob_lo = nullptr, *Ab_lo = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
     float *attn_part = nullptr;
     size_t attn_part_floats = 0;
@@ -179,7 +181,7 @@ SkinnyPlan plan_skinny(int ncols, int K, bool swiglu, const char *env_nt, const 
     SkinnyPlan p;
     p.nt = ncols % 64 == 0 ? 4 : (ncols % 32 == 0 ? 2 : 1);
     const int nt = env_int(env_nt, 0);
-    if ((nt == 1 || nt == 2 || nt == 4) && ncols % (16 * nt) == 0) p.nt = nt;
+    if ((nt == 1 || nt == 2 || nt == 4 || nt == 8) && ncols % (16 * nt) == 0) p.nt = nt;
     if (swiglu && p.nt < 2) p.nt = 2;
     const int tiles = ncols / (16 * p.nt);
     if (swiglu) { p.split = 1; return p; }
@@ -204,23 +206,24 @@ hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
     return launch_linear_simple(c->bf16, epi, a, s);
 }
 
-LinearArgs make_args(const void *x, int ldx, int R, int K, int N, const void *w0, const void *w1, const void *w2,
-                     int e0, int e1, void *out, int ldo) {
+LinearArgs make_args(const void *x, const void *x_lo, int ldx, int R, int K, int N, const void *w0, const void *w1,
+                     const void *w2, int e0, int e1, void *out, void *out_lo, int ldo) {
     LinearArgs a{};
-    a.x = x; a.ldx = ldx; a.R = R; a.K = K; a.N = N;
+    a.x = x; a.x_lo = x_lo; a.ldx = ldx; a.R = R; a.K = K; a.N = N;
+    a.out_lo = out_lo;
     a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
     a.out = out; a.ldo = ldo;
     return a;
 }
 
-hipError_t skinny(int epi, const void *x, int R, int K, int N, const void *w0, const void *w1, const void *w2, int e0,
-                  int e1, void *out, const SkinnyPlan &p, hipStream_t s) {
+hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *w0, const void *w1,
+                  const void *w2, int e0, int e1, void *out, void *out_lo, const SkinnyPlan &p, hipStream_t s) {
     SkinnyArgs a{};
-    a.x = x; a.R = R; a.K = K; a.N = N;
+    a.x = x; a.x_lo = x_lo; a.R = R; a.K = K; a.N = N;
     a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
-    a.out = out; a.split = p.split;
+    a.out = out; a.out_lo = out_lo; a.split = p.split;
     return launch_linear_skinny(epi, a, p.nt, s);
 }
 
@@ -298,50 +301,55 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     int resid_split = 0;  // partial tiles in P still to be added to H
     for (int l = 0; l < d.n_layers; ++l) {
         const kvr_layer_weights &w = c->layers[l];
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, D, sk, s),
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
                   "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Xn, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, p_qkv, s), "qkv",
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, nullptr, p_qkv, s), "qkv",
                       ST_QKV);
             qkv_split = p_qkv.split;
         } else {
-            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, NQKV), s),
+            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, nullptr,
+                                                 NQKV), s),
                       "qkv", ST_QKV);
         }
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
-                                      hd, c->rope_cos, c->rope_sin, c->Qb, s), "rope_scatter", ST_ROPE);
+                                      hd, c->rope_cos, c->rope_sin, c->Qb, c->Qb_lo, s), "rope_scatter", ST_ROPE);
         if (attn_mfma) {
-            KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, rows, docs, items, (int)t.items.size(), l,
-                                            d.n_heads, d.n_kv_heads, c->attn_part, (bf16_t *)c->Ob, sk, s),
+            KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, docs, items,
+                                            (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
+                                            (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, s),
                       "attention", ST_ATTN);
             if (!t.comb.empty())
                 KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
-                                                   (bf16_t *)c->Ob, sk, s), "attention_combine", ST_COMBINE);
+                                                   (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, s), "attention_combine", ST_COMBINE);
         } else {
-            KVR_CHECK(launch_attention_simple(bf, c->Qb, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob, sk, s),
+            KVR_CHECK(launch_attention_simple(bf, c->Qb, c->Qb_lo, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob,
+                                              c->Ob_lo, sk, s),
                       "attention_simple", ST_ATTN);
         }
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Ob, R, qd, D, w.wo, w.wo, w.wo, D, D, c->P, p_o, s), "o_proj", ST_OPROJ);
+            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, w.wo, w.wo, w.wo, D, D, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
             resid_split = p_o.split;
         } else {
-            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, D), s),
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
         }
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, D, sk, s),
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
                   "rmsnorm(mlp)", ST_NORM);
         resid_split = 0;
         if (sk) {
-            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, p_gu, s), "gate_up",
+            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
                       ST_GATEUP);
-            KVR_CHECK(skinny(EPI_STORE, c->Ab, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->P, p_down, s), "down",
+            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->P, nullptr, p_down, s), "down",
                       ST_DOWN);
             resid_split = p_down.split;
         } else {
-            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, F), s),
+            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab,
+                                                  c->Ab_lo, F), s),
                       "gate_up", ST_GATEUP);
-            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H, D), s),
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H,
+                                                 nullptr, D), s),
                       "down", ST_DOWN);
         }
     }
@@ -432,8 +440,11 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
     const size_t p_floats = std::max(R * (qd + 2 * kd), (size_t)SPLIT_MAX * 64 * std::max(qd + 2 * kd, D));
+    const size_t lo_es = c->bf16 ? es : 0;  // compensated low parts exist in bf16 only
     const size_t o_H = take(R * D * 4), o_P = take(p_floats * 4), o_Xn = take(R * D * es),
                  o_Qb = take(R * qd * es), o_Ob = take(R * qd * es), o_Ab = take(R * F * es),
+                 o_Xl = take(R * D * lo_es), o_Ql = take(R * qd * lo_es), o_Ol = take(R * qd * lo_es),
+                 o_Al = take(R * F * lo_es),
                  o_cos = take((size_t)d.max_ctx * (hd / 2) * 4), o_sin = take((size_t)d.max_ctx * (hd / 2) * 4),
                  o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes);
     c->ws_bytes = off;
@@ -445,6 +456,12 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     c->Qb = c->ws + o_Qb;
     c->Ob = c->ws + o_Ob;
     c->Ab = c->ws + o_Ab;
+    if (c->bf16) {
+        c->Xn_lo = c->ws + o_Xl;
+        c->Qb_lo = c->ws + o_Ql;
+        c->Ob_lo = c->ws + o_Ol;
+        c->Ab_lo = c->ws + o_Al;
+    }
     c->rope_cos = (float *)(c->ws + o_cos);
     c->rope_sin = (float *)(c->ws + o_sin);
     c->attn_part = (float *)(c->ws + o_ap);

@@ -4,11 +4,13 @@
 // reading the weights once from HBM: every weight element meets only R rows.
 // Each wavefront streams a 16*NT-row slab of W over a contiguous range of K
 // directly into registers in the B-operand layout of v_mfma_f32_16x16x32_bf16
-// (lane l: weight row l%16, 8 consecutive k at 8*(l/16)); eight k-steps of
-// loads are issued before their MFMAs.  The activations X come in "operand
+// (lane l: weight row l%16, 8 consecutive k at 8*(l/16)); a batch of k-steps
+// of loads is issued before its MFMAs.  The activations X come in "operand
 // order" (see perm_offset in common.h) so that each 16-row A-operand load is one
-// contiguous 1 KB read.  The four wavefronts of a block split the block's K
-// range and are summed through LDS.
+// contiguous 1 KB read; they are compensated pairs (hi + lo), so every
+// (row tile, weight tile) product is two MFMAs into one fp32 accumulator.  The
+// four wavefronts of a block split the block's K range and are summed through
+// LDS.
 //
 // Blocks never exchange data with each other: when K is split over `split`
 // blocks, each writes an fp32 partial tile [split][R][N] and the row-wise
@@ -30,7 +32,7 @@ __device__ __forceinline__ bf16x8 ld16(const bf16_t *p) {
 template <int MT, int NT, int EPI>
 __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     constexpr int FW = 16 * NT;  // output columns of a block
-    constexpr int U = 8;         // k-steps (of 32) per load batch
+    constexpr int U = NT >= 8 ? 2 : 4;  // k-steps (of 32) per load batch
     __shared__ float red[MT * 16][FW];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -61,9 +63,12 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         wp[nt] = base + (size_t)row * K + koff;
     }
     // operand-order X: tile mt, k-step s at ((mt * ksteps + s) * 64 + lane) * 8
-    const bf16_t *xp[MT];
+    const bf16_t *xp[MT], *xq[MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) xp[mt] = (const bf16_t *)a.x + ((size_t)mt * ksteps * 64 + lane) * 8;
+    for (int mt = 0; mt < MT; ++mt) {
+        xp[mt] = (const bf16_t *)a.x + ((size_t)mt * ksteps * 64 + lane) * 8;
+        xq[mt] = (const bf16_t *)a.x_lo + ((size_t)mt * ksteps * 64 + lane) * 8;
+    }
 
     f32x4 acc[MT][NT];
 #pragma unroll
@@ -73,7 +78,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
 
     int s = s0;
     for (; s + U <= s1; s += U) {
-        bf16x8 wv[U][NT], xv[U][MT];
+        bf16x8 wv[U][NT], xv[U][MT], xl[U][MT];
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -81,26 +86,36 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) xv[u][mt] = ld16(xp[mt] + (size_t)(s + u) * 512);
+            for (int mt = 0; mt < MT; ++mt) {
+                xv[u][mt] = ld16(xp[mt] + (size_t)(s + u) * 512);
+                xl[u][mt] = ld16(xq[mt] + (size_t)(s + u) * 512);
+            }
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
+                for (int nt = 0; nt < NT; ++nt) {
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[u][mt], wv[u][nt], acc[mt][nt], 0, 0, 0);
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl[u][mt], wv[u][nt], acc[mt][nt], 0, 0, 0);
+                }
     }
     for (; s < s1; ++s) {
-        bf16x8 wv[NT], xv[MT];
+        bf16x8 wv[NT], xv[MT], xl[MT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) wv[nt] = ld16(wp[nt] + s * 32);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) xv[mt] = ld16(xp[mt] + (size_t)s * 512);
+        for (int mt = 0; mt < MT; ++mt) {
+            xv[mt] = ld16(xp[mt] + (size_t)s * 512);
+            xl[mt] = ld16(xq[mt] + (size_t)s * 512);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
+            for (int nt = 0; nt < NT; ++nt) {
                 acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[mt], wv[nt], acc[mt][nt], 0, 0, 0);
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl[mt], wv[nt], acc[mt][nt], 0, 0, 0);
+            }
     }
 
     // sum the four wavefronts in a fixed order; accumulator layout: lane l holds
@@ -124,9 +139,10 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     if (EPI == EPI_SWIGLU) {
         constexpr int FH = FW / 2;
         bf16_t *A = (bf16_t *)a.out;
+        bf16_t *Al = (bf16_t *)a.out_lo;
         for (int i = threadIdx.x; i < R * FH; i += 256) {
             const int r = i / FH, f = i - r * FH;
-            A[perm_offset(r, tile * FH + f, a.N)] = f32_to_bf16(silu_f(red[r][f]) * red[r][FH + f]);
+            store_operand(A, Al, perm_offset(r, tile * FH + f, a.N), silu_f(red[r][f]) * red[r][FH + f]);
         }
     } else {
         float *out = (float *)a.out + (size_t)sp * R * a.N;
@@ -162,12 +178,14 @@ hipError_t launch_nt(int epi, const SkinnyArgs &a, hipStream_t s) {
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s) {
     if (a.R <= 0) return hipSuccess;
     const int ncols = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+    if (!a.x_lo || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
     if (a.R > 64 || a.K % 32 != 0 || a.split < 1 || (epi == EPI_SWIGLU && a.split != 1) ||
-        (nt != 1 && nt != 2 && nt != 4) || ncols % (16 * nt) != 0 || (epi == EPI_SWIGLU && nt < 2))
+        (nt != 1 && nt != 2 && nt != 4 && nt != 8) || ncols % (16 * nt) != 0 || (epi == EPI_SWIGLU && nt < 2))
         return hipErrorInvalidValue;
     if (nt == 1) return launch_nt<1>(epi, a, s);
     if (nt == 2) return launch_nt<2>(epi, a, s);
-    return launch_nt<4>(epi, a, s);
+    if (nt == 4) return launch_nt<4>(epi, a, s);
+    return launch_nt<8>(epi, a, s);
 }
 
 }  // namespace kvr

@@ -4,8 +4,10 @@
 // 128x128 output tile streams 64-wide K slabs of X and W through LDS (rows
 // padded to 144 B so that the 16-byte operand reads of a wavefront spread over
 // the banks), and each of the four wavefronts computes a 64x64 sub-tile as
-// 4x4 v_mfma_f32_16x16x32_bf16 tiles.  The next slab is fetched into
-// registers while the current one is multiplied.
+// 4x4 v_mfma_f32_16x16x32_bf16 tiles.  X is a compensated pair (hi + lo), so
+// its slab is staged twice and every product is two MFMAs into one fp32
+// accumulator.  The next slab is fetched into registers while the current one
+// is multiplied.
 #include "common.h"
 
 namespace kvr {
@@ -20,6 +22,7 @@ __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)
 template <int EPI>
 __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
     __shared__ __attribute__((aligned(16))) bf16_t As[BM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) bf16_t Al[BM * LDS_STRIDE];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[BN * LDS_STRIDE];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -29,12 +32,13 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
 
     // global -> register loader: thread covers rows tid/8 + 32*i, 16 bytes at k (tid%8)*8
     const int lrow = tid >> 3, lk = (tid & 7) * 8;
-    const bf16_t *ag[4];
+    const bf16_t *ag[4], *al[4];
     const bf16_t *bg[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = min(bm * BM + lrow + 32 * i, a.R - 1);
         ag[i] = (const bf16_t *)a.x + (size_t)r * a.ldx + lk;
+        al[i] = (const bf16_t *)a.x_lo + (size_t)r * a.ldx + lk;
         const int c = lrow + 32 * i;  // B-tile row (output column of the tile)
         const bf16_t *base;
         int row;
@@ -51,10 +55,11 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
         bg[i] = base + (size_t)row * K + lk;
     }
 
-    u32x4 ra[4], rb[4];
+    u32x4 ra[4], rl[4], rb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         ra[i] = *reinterpret_cast<const u32x4 *>(ag[i]);
+        rl[i] = *reinterpret_cast<const u32x4 *>(al[i]);
         rb[i] = *reinterpret_cast<const u32x4 *>(bg[i]);
     }
 
@@ -70,6 +75,7 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             *reinterpret_cast<u32x4 *>(&As[(lrow + 32 * i) * LDS_STRIDE + lk]) = ra[i];
+            *reinterpret_cast<u32x4 *>(&Al[(lrow + 32 * i) * LDS_STRIDE + lk]) = rl[i];
             *reinterpret_cast<u32x4 *>(&Bs[(lrow + 32 * i) * LDS_STRIDE + lk]) = rb[i];
         }
         __syncthreads();
@@ -77,22 +83,26 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 ra[i] = *reinterpret_cast<const u32x4 *>(ag[i] + k0 + BK);
+                rl[i] = *reinterpret_cast<const u32x4 *>(al[i] + k0 + BK);
                 rb[i] = *reinterpret_cast<const u32x4 *>(bg[i] + k0 + BK);
             }
         }
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
-            bf16x8 av[4], bv[4];
+            bf16x8 av[4], avl[4], bv[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 av[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * 64 + i * 16 + (lane & 15)) * LDS_STRIDE + ks * 32 + koff]);
+                avl[i] = *reinterpret_cast<const bf16x8 *>(&Al[(wm * 64 + i * 16 + (lane & 15)) * LDS_STRIDE + ks * 32 + koff]);
                 bv[i] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * 64 + i * 16 + (lane & 15)) * LDS_STRIDE + ks * 32 + koff]);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < 4; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avl[i], bv[j], acc[i][j], 0, 0, 0);
+                }
         }
     }
 
@@ -100,6 +110,7 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
     const int rbase = bm * BM + wm * 64 + 4 * (lane >> 4);
     if (EPI == EPI_SWIGLU) {
         bf16_t *A = (bf16_t *)a.out;
+        bf16_t *Alo = (bf16_t *)a.out_lo;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -109,7 +120,7 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     const int f = bn * 64 + wn * 32 + j * 16 + (lane & 15);
-                    A[(size_t)r * a.ldo + f] = f32_to_bf16(silu_f(acc[i][j][e]) * acc[i][j + 2][e]);
+                    store_operand(A, Alo, (size_t)r * a.ldo + f, silu_f(acc[i][j][e]) * acc[i][j + 2][e]);
                 }
             }
         return;
@@ -134,6 +145,7 @@ __global__ __launch_bounds__(256) void linear_tiled_kernel(LinearArgs a) {
 
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     if (a.R <= 0) return hipSuccess;
+    if (!a.x_lo || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
     const int nb = epi == EPI_SWIGLU ? a.N / 64 : a.N / BN;
     dim3 grid(nb, (a.R + BM - 1) / BM);
     if (epi == EPI_STORE) hipLaunchKernelGGL(linear_tiled_kernel<EPI_STORE>, grid, dim3(256), 0, s, a);

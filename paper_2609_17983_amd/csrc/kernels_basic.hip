@@ -73,7 +73,7 @@ __device__ __forceinline__ float4 add_partials(float4 h, const float *part, int 
 // per pass (d % 4 == 0).
 template <typename TO, typename TG, bool PERM>
 __global__ __launch_bounds__(1024) void rmsnorm_kernel(float *H, const float *part, int nsplit, int R,
-                                                       const TG *gain, int d, float eps, TO *X, int ldx) {
+                                                       const TG *gain, int d, float eps, TO *X, TO *X_lo, int ldx) {
     __shared__ float red[16];
     const int r = blockIdx.x;
     float *h = H + (size_t)r * d;
@@ -94,9 +94,7 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(float *H, const float *pa
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int c = 4 * i + e;
-            const TO y = from_f32<TO>(vv[e] * inv * to_f32(gain[c]));
-            if (PERM) X[perm_offset(r, c, d)] = y;
-            else X[(size_t)r * ldx + c] = y;
+            store_operand(X, X_lo, PERM ? perm_offset(r, c, d) : (size_t)r * ldx + c, vv[e] * inv * to_f32(gain[c]));
         }
     }
 }
@@ -141,7 +139,7 @@ template <typename T>
 __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, int nsplit, int R, const T *bq,
                                                            const T *bk, const T *bv, const RowInfo *rows,
                                                            const DocInfo *docs, int layer, int Hq, int Hkv, int hd,
-                                                           const float *rcos, const float *rsin, T *Q) {
+                                                           const float *rcos, const float *rsin, T *Q, T *Q_lo) {
     const int r = blockIdx.x;
     const RowInfo ri = rows[r];
     const DocInfo dc = docs[ri.doc];
@@ -178,8 +176,8 @@ __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, in
         const float c = cs[i], s = sn[i];
         const float o1 = a * c - b * s, o2 = b * c + a * s;
         if (j < Hq) {
-            Q[(size_t)r * qd + j * hd + i] = from_f32<T>(o1);
-            Q[(size_t)r * qd + j * hd + i + half] = from_f32<T>(o2);
+            store_operand(Q, Q_lo, (size_t)r * qd + j * hd + i, o1);
+            store_operand(Q, Q_lo, (size_t)r * qd + j * hd + i + half, o2);
         } else {
             const int g = j - Hq;
             kbase[g * head_stride + i] = from_f32<T>(o1);
@@ -196,8 +194,9 @@ __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, in
 
 // One wavefront per (row, query head): online softmax over keys 0..pos.
 template <typename T>
-__global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const RowInfo *rows, const DocInfo *docs,
-                                                              int layer, int Hq, int Hkv, int hd, T *O, int o_perm) {
+__global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const T *Q_lo, const RowInfo *rows,
+                                                              const DocInfo *docs, int layer, int Hq, int Hkv, int hd,
+                                                              T *O, T *O_lo, int o_perm) {
     const int r = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
     const RowInfo ri = rows[r];
     const DocInfo dc = docs[ri.doc];
@@ -208,8 +207,8 @@ __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const 
     const int qd = Hq * hd;
     const bool has0 = lane < hd, has1 = lane + 64 < hd;
     const float scale = 1.0f / sqrtf((float)hd);
-    const float q0 = has0 ? to_f32(Q[(size_t)r * qd + j * hd + lane]) * scale : 0.f;
-    const float q1 = has1 ? to_f32(Q[(size_t)r * qd + j * hd + lane + 64]) * scale : 0.f;
+    const float q0 = has0 ? load_operand(Q, Q_lo, (size_t)r * qd + j * hd + lane) * scale : 0.f;
+    const float q1 = has1 ? load_operand(Q, Q_lo, (size_t)r * qd + j * hd + lane + 64) * scale : 0.f;
     float m = -INFINITY, l = 0.f, a0 = 0.f, a1 = 0.f;
     for (int t = 0; t <= ri.pos; ++t) {
         const T *kr = K + (size_t)t * hd;
@@ -225,9 +224,10 @@ __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const 
         m = mn;
     }
     const float inv = 1.0f / l;
-    if (has0) O[o_perm ? perm_offset(r, j * hd + lane, qd) : (size_t)r * qd + j * hd + lane] = from_f32<T>(a0 * inv);
+    if (has0) store_operand(O, O_lo, o_perm ? perm_offset(r, j * hd + lane, qd) : (size_t)r * qd + j * hd + lane, a0 * inv);
     if (has1)
-        O[o_perm ? perm_offset(r, j * hd + lane + 64, qd) : (size_t)r * qd + j * hd + lane + 64] = from_f32<T>(a1 * inv);
+        store_operand(O, O_lo, o_perm ? perm_offset(r, j * hd + lane + 64, qd) : (size_t)r * qd + j * hd + lane + 64,
+                      a1 * inv);
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
@@ -243,6 +243,7 @@ __global__ __launch_bounds__(256) void linear_simple_kernel(LinearArgs a) {
     const int r0 = blockIdx.y * 64;
     const int c0 = blockIdx.x * 64;
     const T *X = (const T *)a.x;
+    const T *Xl = (const T *)a.x_lo;
     // weight row pointer of the tile's column c (0..63); null if out of range
     auto wrow = [&](int c) -> const T * {
         if (EPI == EPI_SWIGLU) {
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(256) void linear_simple_kernel(LinearArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int k = k0 + lk + e;
-            xs[lk + e][lr] = (xr < a.R && k < a.K) ? to_f32(X[(size_t)xr * a.ldx + k]) : 0.f;
+            xs[lk + e][lr] = (xr < a.R && k < a.K) ? load_operand(X, Xl, (size_t)xr * a.ldx + k) : 0.f;
             ws[lk + e][lr] = (wr && k < a.K) ? to_f32(wr[k]) : 0.f;
         }
         __syncthreads();
@@ -288,11 +289,12 @@ __global__ __launch_bounds__(256) void linear_simple_kernel(LinearArgs a) {
             for (int jj = 0; jj < 4; ++jj) tile[ty * 4 + i][tx * 4 + jj] = acc[i][jj];
         __syncthreads();
         T *A = (T *)a.out;
+        T *Al = (T *)a.out_lo;
         for (int idx = threadIdx.x; idx < 64 * 32; idx += 256) {
             const int rr = idx >> 5, f = idx & 31;
             const int row = r0 + rr, feat = blockIdx.x * 32 + f;
             if (row < a.R && feat < a.N)
-                A[(size_t)row * a.ldo + feat] = from_f32<T>(silu_f(tile[rr][f]) * tile[rr][32 + f]);
+                store_operand(A, Al, (size_t)row * a.ldo + feat, silu_f(tile[rr][f]) * tile[rr][32 + f]);
         }
         return;
     }
@@ -326,19 +328,19 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
 }
 
 hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
-                          int R, int d, float eps, void *X, int ldx, bool perm, hipStream_t s) {
+                          int R, int d, float eps, void *X, void *X_lo, int ldx, bool perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (d % 4 != 0) return hipErrorInvalidValue;
     if (bf16_out && bf16_gain) {
         if (perm)
             hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, true>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
-                               (const bf16_t *)gain, d, eps, (bf16_t *)X, ldx);
+                               (const bf16_t *)gain, d, eps, (bf16_t *)X, (bf16_t *)X_lo, ldx);
         else
             hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
-                               (const bf16_t *)gain, d, eps, (bf16_t *)X, ldx);
+                               (const bf16_t *)gain, d, eps, (bf16_t *)X, (bf16_t *)X_lo, ldx);
     } else if (!bf16_out && !bf16_gain && !perm) {
         hipLaunchKernelGGL((rmsnorm_kernel<float, float, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
-                           (const float *)gain, d, eps, (float *)X, ldx);
+                           (const float *)gain, d, eps, (float *)X, (float *)nullptr, ldx);
     } else {
         return hipErrorInvalidValue;
     }
@@ -360,7 +362,7 @@ hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int ns
 
 hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const void *bq, const void *bk,
                                const void *bv, const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq,
-                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q,
+                               int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q, void *Q_lo,
                                hipStream_t s) {
     if (R <= 0) return hipSuccess;
     const size_t lds = (size_t)(Hq + 2 * Hkv) * hd * sizeof(float);
@@ -368,23 +370,24 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
     if (bf16)
         hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
                            (const bf16_t *)bq, (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd,
-                           rope_cos, rope_sin, (bf16_t *)Q);
+                           rope_cos, rope_sin, (bf16_t *)Q, (bf16_t *)Q_lo);
     else
         hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
                            (const float *)bq, (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd,
-                           rope_cos, rope_sin, (float *)Q);
+                           rope_cos, rope_sin, (float *)Q, (float *)nullptr);
     return hipGetLastError();
 }
 
-hipError_t launch_attention_simple(bool bf16, const void *Q, const RowInfo *rows, const DocInfo *docs, int R,
-                                   int layer, int Hq, int Hkv, int hd, void *O, bool o_perm, hipStream_t s) {
+hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, const RowInfo *rows,
+                                   const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd, void *O, void *O_lo,
+                                   bool o_perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (bf16)
-        hipLaunchKernelGGL(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q, rows, docs,
-                           layer, Hq, Hkv, hd, (bf16_t *)O, (int)o_perm);
+        hipLaunchKernelGGL(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q,
+                           (const bf16_t *)Q_lo, rows, docs, layer, Hq, Hkv, hd, (bf16_t *)O, (bf16_t *)O_lo, (int)o_perm);
     else if (!o_perm)
-        hipLaunchKernelGGL(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q, rows, docs,
-                           layer, Hq, Hkv, hd, (float *)O, 0);
+        hipLaunchKernelGGL(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q,
+                           (const float *)nullptr, rows, docs, layer, Hq, Hkv, hd, (float *)O, (float *)nullptr, 0);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
