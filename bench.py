@@ -49,8 +49,10 @@ def parse():
     ap.add_argument("--prefill-steps", type=int, default=5)
     ap.add_argument("--profile-steps", type=int, default=5,
                     help="repairs run with per-launch event profiling after the timed loop")
-    ap.add_argument("--cpu-layers", type=int, default=8,
+    ap.add_argument("--cpu-layers", type=int, default=32,
                     help="layers of the repair the CPU oracle runs for its bounded sample")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 1 GiB device-to-device copy first (reference for HBM byte counters)")
     ap.add_argument("--no-cpu", action="store_true")
     return ap.parse_args()
 
@@ -95,6 +97,13 @@ def main():
     stream = torch.cuda.current_stream()
 
     log(f"workload {args.workload}: {shape.name}, n={n}, edit [{e},{e + span}), {wl['policy']} K={K} -> {R} rows")
+    if args.calibrate_copy:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration copy: 1 GiB read + 1 GiB written")
+        del src, dst
     w = synth.make_weights(shape, dtype=torch.bfloat16, device="cuda")
     dims = kvr.dims_for(shape, kvr.KVR_BF16, max_ctx=n, max_rows=max(R, 64))
     ws = kvr.weights_struct(w)
@@ -161,12 +170,15 @@ def main():
     log(f"gate/up+SwiGLU kernel: {kern_ms * 1e3:.1f} us/launch, {kern_gbs:.0f} GB/s")
 
     traffic = None
-    tfile = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_gateup_llama8b_r48.json")
-    if os.path.exists(tfile):
+    # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE counter passes, valid
+    # only while the kernel source is the one the counters were taken on
+    tfile = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                         "gateup_swiglu_llama8b_r48_traffic.md")
+    if wl["shape"] == "llama3-8b" and R == 48 and os.path.exists(tfile):
         with open(tfile) as f:
-            tj = json.load(f)
-        if tj.get("kernel_source_sha") == _kernel_sha():
-            traffic = tj.get("hbm_bytes_per_launch")
+            kv = dict(l.split(": ", 1) for l in f.read().splitlines() if l.startswith(("hbm_bytes", "kernel_source")))
+        if kv.get("kernel_source_sha") == _kernel_sha():
+            traffic = int(kv["hbm_bytes_per_launch"])
 
     # ---- fp64 CPU oracle on a bounded sample of the same repair
     cpu = None
