@@ -106,23 +106,24 @@ struct LinearArgs {
     const void *x_lo;     // low part of a compensated bf16 operand, or null
     int32_t ldx;
     int32_t R, K, N;      // N: output columns (SWIGLU: number of features f)
-    const void *w[3];     // row blocks of W
+    const void *w[3];     // row-major row blocks of W (simple kernel)
     int32_t seg_end[3];   // cumulative output-column boundaries of the blocks
+    const void *wp;       // W packed in operand order (tiled kernel; pack.hip)
     void *out;            // STORE: float [R][ldo]; RESID: float [R][ldo] (+=);
                           // SWIGLU: operand type [R][ldo]
     void *out_lo;         // SWIGLU: low part of the compensated output, or null
     int32_t ldo;
-    float *partial;       // split-K scratch
-    int32_t *counters;    // split-K tile counters (kept at zero between calls)
 };
 
-// Skinny (R <= 64) linear layer: X in operand order; STORE writes fp32 partial
-// tiles [split][R][N]; SWIGLU (split 1) writes silu(gate)*up in operand order.
+// Skinny (R <= 64) linear layer: X in operand order, W packed in operand order
+// with ntiles 16-row tiles (SWIGLU: gate/up interleaved, 2N virtual rows);
+// STORE writes fp32 partial tiles [split][R][N]; SWIGLU (split 1) writes
+// silu(gate)*up in operand order.
 struct SkinnyArgs {
     const void *x, *x_lo;  // compensated operand (hi, lo), both in operand order
     int32_t R, K, N;      // N: output columns (SWIGLU: number of features)
-    const void *w[3];
-    int32_t seg_end[3];
+    const void *w;         // packed weight
+    int32_t ntiles;
     void *out, *out_lo;    // SWIGLU writes a compensated pair
     int32_t split;
 };
@@ -157,10 +158,15 @@ hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowI
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
                                     int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s);
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
-// Skinny MFMA path (R <= 64); nt = 16-row weight tiles per wave (1, 2 or 4).
+// Skinny MFMA path (R <= 64); nt = 16-row weight tiles per block (1..8).
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s);
-// Tiled MFMA path for many rows.
+// Tiled MFMA path for many rows (packed weight, K a multiple of 64).
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
+// Repack up to three row-major bf16 matrices (rows [0,e0), [e0,e1), [e1,V) of
+// the virtual matrix; interleave: w0 = gate, w1 = up, tile t = gate rows
+// 8t..8t+7 then up rows 8t..8t+7) of K columns into operand order at dst.
+hipError_t launch_pack_weight(const void *w0, const void *w1, const void *w2, int e0, int e1, bool interleave,
+                              int V, int K, void *dst, hipStream_t s);
 
 // Attention item geometry shared by the planner and the kernels.
 constexpr int ATT_KT = 64;     // keys per LDS tile

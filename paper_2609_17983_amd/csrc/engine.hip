@@ -36,6 +36,12 @@ struct kvr_ctx {
     std::vector<kvr_layer_weights> layers;
     const void *embed = nullptr, *final_norm = nullptr;
 
+    // projection weights repacked in operand order (bf16 MFMA paths)
+    struct PackedLayer { const void *qkv, *o, *gu, *down; };
+    std::vector<PackedLayer> pk;
+    char *wpk = nullptr;
+    size_t wpk_bytes = 0;
+
     int rows_cap = 0;  // rows per pass
     int max_docs = 0;
     int items_cap = 0, comb_cap = 0;
@@ -173,56 +179,59 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
                      [](const AttnItem &x, const AttnItem &y) { return (x.k1 - x.k0) > (y.k1 - y.k0); });
 }
 
-// Weight tiles per wavefront and split-K factor of a skinny projection: about
-// 512 blocks, at least 8 k-steps of 32 per wavefront, never split for SwiGLU.
+// Weight tiles per block and split-K factor of a skinny projection.  The X
+// operand is re-read from L2 once per block column, so blocks are made as wide
+// as the grid allows: the K slice of each wavefront is 8-16 k-steps (split a
+// power of two, never split for SwiGLU) and NT = ceil(ntiles * split / 256)
+// tiles (at most 8) gives about one block per compute unit.
 struct SkinnyPlan { int nt, split; };
 
-SkinnyPlan plan_skinny(int ncols, int K, bool swiglu, const char *env_nt, const char *env_split) {
-    SkinnyPlan p;
-    p.nt = ncols % 64 == 0 ? 4 : (ncols % 32 == 0 ? 2 : 1);
+SkinnyPlan plan_skinny(int ntiles, int K, bool swiglu, const char *env_nt, const char *env_split) {
+    const int ksteps = K / 32;
+    SkinnyPlan p{1, 1};
+    if (!swiglu)
+        while (p.split * 2 <= SPLIT_MAX && ksteps / (4 * p.split) > 16 && ksteps / (8 * p.split) >= 8) p.split *= 2;
+    const int es = env_split ? env_int(env_split, 0) : 0;
+    if (!swiglu && es >= 1) p.split = std::min(es, std::min(SPLIT_MAX, ksteps));
+    p.nt = std::max(1, std::min(8, (ntiles * p.split + 255) / 256));
     const int nt = env_int(env_nt, 0);
-    if ((nt == 1 || nt == 2 || nt == 4 || nt == 8) && ncols % (16 * nt) == 0) p.nt = nt;
-    if (swiglu && p.nt < 2) p.nt = 2;
-    const int tiles = ncols / (16 * p.nt);
-    if (swiglu) { p.split = 1; return p; }
-    const int smax = std::max(1, std::min(SPLIT_MAX, (K / 32) / 32));
-    p.split = std::max(1, std::min(smax, (512 + tiles - 1) / tiles));
-    const int es = env_int(env_split, 0);
-    if (es >= 1) p.split = std::min(es, std::min(SPLIT_MAX, K / 32));
+    if (nt >= 1 && nt <= 8) p.nt = nt;
     return p;
 }
 
-bool skinny_pass_ok(const kvr_ctx *c, int R) {
-    const kvr_dims &d = c->d;
+// Shapes the packed-weight MFMA kernels take (K of every projection a multiple
+// of 64, weight tiles of 16 rows).
+bool pack_ok(const kvr_dims &d, bool force_simple) {
     const int qd = d.n_heads * d.head_dim, kd = d.n_kv_heads * d.head_dim;
-    return c->bf16 && !c->force_simple && R <= 64 && d.d_model % 32 == 0 && qd % 32 == 0 && d.d_ffn % 32 == 0 &&
-           (qd + 2 * kd) % 16 == 0 && d.d_model % 16 == 0;
+    return d.dtype == KVR_BF16 && !force_simple && d.d_model % 64 == 0 && qd % 64 == 0 && d.d_ffn % 64 == 0 &&
+           kd % 16 == 0;
 }
 
+bool skinny_pass_ok(const kvr_ctx *c, int R) { return c->wpk != nullptr && R <= 64; }
+
 hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
-    if (!c->bf16 || c->force_simple) return launch_linear_simple(c->bf16, epi, a, s);
-    if (a.K % 64 == 0 && a.ldx % 8 == 0 && (epi == EPI_SWIGLU ? a.N % 64 == 0 : a.N % 128 == 0))
-        return launch_linear_tiled(epi, a, s);
+    if (a.wp && a.ldx % 8 == 0) return launch_linear_tiled(epi, a, s);
     return launch_linear_simple(c->bf16, epi, a, s);
 }
 
 LinearArgs make_args(const void *x, const void *x_lo, int ldx, int R, int K, int N, const void *w0, const void *w1,
-                     const void *w2, int e0, int e1, void *out, void *out_lo, int ldo) {
+                     const void *w2, int e0, int e1, const void *wp, void *out, void *out_lo, int ldo) {
     LinearArgs a{};
     a.x = x; a.x_lo = x_lo; a.ldx = ldx; a.R = R; a.K = K; a.N = N;
     a.out_lo = out_lo;
     a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
+    a.wp = wp;
     a.out = out; a.ldo = ldo;
     return a;
 }
 
-hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *w0, const void *w1,
-                  const void *w2, int e0, int e1, void *out, void *out_lo, const SkinnyPlan &p, hipStream_t s) {
+hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *wp, void *out,
+                  void *out_lo, const SkinnyPlan &p, hipStream_t s) {
     SkinnyArgs a{};
     a.x = x; a.x_lo = x_lo; a.R = R; a.K = K; a.N = N;
-    a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
-    a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
+    a.w = wp;
+    a.ntiles = (epi == EPI_SWIGLU ? 2 * N : N) / 16;
     a.out = out; a.out_lo = out_lo; a.split = p.split;
     return launch_linear_skinny(epi, a, p.nt, s);
 }
@@ -284,10 +293,10 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     const bool bf = c->bf16;
     SkinnyPlan p_qkv{}, p_o{}, p_gu{}, p_down{};
     if (sk) {
-        p_qkv = plan_skinny(NQKV, D, false, "KVR_NT_QKV", "KVR_SPLIT_QKV");
-        p_o = plan_skinny(D, qd, false, "KVR_NT_O", "KVR_SPLIT_O");
-        p_gu = plan_skinny(2 * F, D, true, "KVR_NT_GATEUP", nullptr);
-        p_down = plan_skinny(D, F, false, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
+        p_qkv = plan_skinny(NQKV / 16, D, false, "KVR_NT_QKV", "KVR_SPLIT_QKV");
+        p_o = plan_skinny(D / 16, qd, false, "KVR_NT_O", "KVR_SPLIT_O");
+        p_gu = plan_skinny(2 * F / 16, D, true, "KVR_NT_GATEUP", nullptr);
+        p_down = plan_skinny(D / 16, F, false, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
     }
 #define KVR_CHECK(expr, what, step)                                  \
     do {                                                             \
@@ -301,16 +310,17 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     int resid_split = 0;  // partial tiles in P still to be added to H
     for (int l = 0; l < d.n_layers; ++l) {
         const kvr_layer_weights &w = c->layers[l];
+        const kvr_ctx::PackedLayer pw = c->wpk ? c->pk[l] : kvr_ctx::PackedLayer{nullptr, nullptr, nullptr, nullptr};
         KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
                   "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, nullptr, p_qkv, s), "qkv",
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, c->P, nullptr, p_qkv, s), "qkv",
                       ST_QKV);
             qkv_split = p_qkv.split;
         } else {
-            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, c->P, nullptr,
-                                                 NQKV), s),
+            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P,
+                                                 nullptr, NQKV), s),
                       "qkv", ST_QKV);
         }
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
@@ -329,27 +339,27 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
                       "attention_simple", ST_ATTN);
         }
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, w.wo, w.wo, w.wo, D, D, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
+            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
             resid_split = p_o.split;
         } else {
-            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, c->H, nullptr, D), s),
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
         }
         KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
                   "rmsnorm(mlp)", ST_NORM);
         resid_split = 0;
         if (sk) {
-            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
+            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
                       ST_GATEUP);
-            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->P, nullptr, p_down, s), "down",
+            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, c->P, nullptr, p_down, s), "down",
                       ST_DOWN);
             resid_split = p_down.split;
         } else {
-            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, c->Ab,
-                                                  c->Ab_lo, F), s),
+            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu,
+                                                  c->Ab, c->Ab_lo, F), s),
                       "gate_up", ST_GATEUP);
-            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, c->H,
-                                                 nullptr, D), s),
+            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down,
+                                                 c->H, nullptr, D), s),
                       "down", ST_DOWN);
         }
     }
@@ -380,7 +390,7 @@ size_t kvr_cache_bytes(const kvr_dims *d, int32_t n_cap) {
     return (size_t)d->n_layers * 2 * d->n_kv_heads * (size_t)n_cap * d->head_dim * elem_size(*d);
 }
 
-size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes : 0; }
+size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes + c->wpk_bytes : 0; }
 
 const char *kvr_last_error(const kvr_ctx *c) { return c ? c->err.c_str() : g_error.c_str(); }
 
@@ -491,6 +501,42 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
             return hip_fail(nullptr, e, "kvr_create: workspace initialisation");
         }
     }
+    // projection weights in operand order, one contiguous copy per layer
+    if (pack_ok(d, c->force_simple)) {
+        const int NQKV = qd + 2 * kd;
+        const size_t per_layer = (size_t)NQKV * D + (size_t)D * qd + (size_t)2 * F * D + (size_t)D * F;
+        c->wpk_bytes = per_layer * 2 * d.n_layers;
+        e = hipMalloc((void **)&c->wpk, c->wpk_bytes);
+        if (e != hipSuccess) {
+            c->wpk = nullptr;
+            (void)hipEventDestroy(c->stage_ev); (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c;
+            return fail(nullptr, KVR_E_NOMEM, "kvr_create: packed weight allocation failed");
+        }
+        c->pk.resize(d.n_layers);
+        bf16_t *dst = (bf16_t *)c->wpk;
+        for (int l = 0; l < d.n_layers && e == hipSuccess; ++l) {
+            const kvr_layer_weights &w = c->layers[l];
+            kvr_ctx::PackedLayer &pl = c->pk[l];
+            pl.qkv = dst;
+            e = launch_pack_weight(w.wq, w.wk, w.wv, qd, qd + kd, false, NQKV, D, dst, 0);
+            dst += (size_t)NQKV * D;
+            pl.o = dst;
+            if (e == hipSuccess) e = launch_pack_weight(w.wo, w.wo, w.wo, D, D, false, D, qd, dst, 0);
+            dst += (size_t)D * qd;
+            pl.gu = dst;
+            if (e == hipSuccess) e = launch_pack_weight(w.w_gate, w.w_up, w.w_up, F, 2 * F, true, 2 * F, D, dst, 0);
+            dst += (size_t)2 * F * D;
+            pl.down = dst;
+            if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, dst, 0);
+            dst += (size_t)D * F;
+        }
+        if (e == hipSuccess) e = hipStreamSynchronize(0);
+        if (e != hipSuccess) {
+            (void)hipFree(c->wpk);
+            (void)hipEventDestroy(c->stage_ev); (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c;
+            return hip_fail(nullptr, e, "kvr_create: weight packing");
+        }
+    }
     *out = c;
     return KVR_OK;
 }
@@ -505,6 +551,7 @@ void kvr_destroy(kvr_ctx *c) {
         for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
         if (c->h_stage) (void)hipHostFree(c->h_stage);
         if (c->ws) (void)hipFree(c->ws);
+        if (c->wpk) (void)hipFree(c->wpk);
     }
     delete c;
 }

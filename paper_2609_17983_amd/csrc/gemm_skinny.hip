@@ -2,21 +2,28 @@
 //
 // With a repair budget of a few dozen rows the projections are bound by
 // reading the weights once from HBM: every weight element meets only R rows.
-// Each wavefront streams a 16*NT-row slab of W over a contiguous range of K
-// directly into registers in the B-operand layout of v_mfma_f32_16x16x32_bf16
-// (lane l: weight row l%16, 8 consecutive k at 8*(l/16)); a batch of k-steps
-// of loads is issued before its MFMAs.  The activations X come in "operand
-// order" (see perm_offset in common.h) so that each 16-row A-operand load is one
-// contiguous 1 KB read; they are compensated pairs (hi + lo), so every
-// (row tile, weight tile) product is two MFMAs into one fp32 accumulator.  The
-// four wavefronts of a block split the block's K range and are summed through
-// LDS.
+// The weights are packed in operand order (pack.hip), so a wavefront's load of
+// one 16-row x 32-k weight tile is one contiguous 1 KB block that lands in the
+// B-operand layout of v_mfma_f32_16x16x32_bf16 (lane l: weight row l%16, 8
+// consecutive k at 8*(l/16)).  The activations X come in the same operand
+// order, as compensated pairs (hi + lo), so every (row tile, weight tile)
+// product is two MFMAs into one fp32 accumulator.
 //
-// Blocks never exchange data with each other: when K is split over `split`
-// blocks, each writes an fp32 partial tile [split][R][N] and the row-wise
-// kernel that runs next sums the partials in a fixed order (deterministic, and
-// free of device-wide fences).  The gate/up projection is never split; it
-// applies SwiGLU in its epilogue and writes the down projection's operand.
+// A block owns NT consecutive 16-row weight tiles and one of `split` slices of
+// K; its four wavefronts split that slice further and are summed through LDS
+// at the end.  A wide block lets one X read serve NT tiles (X traffic from L2
+// falls as 1/NT), and the planner sizes NT and split so that the grid is about
+// one block per compute unit.  Each wavefront keeps a ring of D k-steps of
+// loads in flight: it consumes one k-step and immediately refills that slot
+// with the k-step D further on, so the memory pipe never drains between
+// batches.
+//
+// Blocks never exchange data: with split > 1 each block writes an fp32 partial
+// tile [split][R][N] and the row-wise kernel that runs next sums the partials
+// in a fixed order (deterministic, and free of device-wide fences).  The
+// gate/up projection is never split; its weight is gate/up interleaved (tile t
+// = gate rows 8t..8t+7, then up rows 8t..8t+7) and the epilogue applies
+// SwiGLU, writing the down projection's operand.
 #include "common.h"
 
 namespace kvr {
@@ -31,38 +38,24 @@ __device__ __forceinline__ bf16x8 ld16(const bf16_t *p) {
 
 template <int MT, int NT, int EPI>
 __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
-    constexpr int FW = 16 * NT;  // output columns of a block
-    constexpr int U = NT >= 8 ? 2 : 4;  // k-steps (of 32) per load batch
+    constexpr int FW = 16 * NT;          // virtual weight rows of a block
+    constexpr int D = NT >= 6 ? 2 : 3;   // k-steps in flight per wavefront
     __shared__ float red[MT * 16][FW];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int split = a.split;
-    const int tile = blockIdx.x / split, sp = blockIdx.x - tile * split;
-    const int K = a.K;
-    const int ksteps = K >> 5;
+    const int tg = blockIdx.x / split, sp = blockIdx.x - tg * split;
+    const int ksteps = a.K >> 5;
     const int gw = sp * 4 + w, nw = split * 4;
     const int s0 = (int)(((long long)ksteps * gw) / nw);
     const int s1 = (int)(((long long)ksteps * (gw + 1)) / nw);
 
-    const int koff = 8 * (lane >> 4);
+    // tiles past the end (last block of a ragged grid) re-read the last tile;
+    // their results are never stored
     const bf16_t *wp[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        const int c = nt * 16 + (lane & 15);
-        const bf16_t *base;
-        int row;
-        if (EPI == EPI_SWIGLU) {
-            base = (const bf16_t *)a.w[nt < NT / 2 ? 0 : 1];
-            row = tile * (FW / 2) + (c & (FW / 2 - 1));
-        } else {
-            const int n = tile * FW + c;
-            if (n < a.seg_end[0]) { base = (const bf16_t *)a.w[0]; row = n; }
-            else if (n < a.seg_end[1]) { base = (const bf16_t *)a.w[1]; row = n - a.seg_end[0]; }
-            else { base = (const bf16_t *)a.w[2]; row = n - a.seg_end[1]; }
-        }
-        wp[nt] = base + (size_t)row * K + koff;
-    }
-    // operand-order X: tile mt, k-step s at ((mt * ksteps + s) * 64 + lane) * 8
+    for (int nt = 0; nt < NT; ++nt)
+        wp[nt] = (const bf16_t *)a.w + ((size_t)min(tg * NT + nt, a.ntiles - 1) * ksteps * 64 + lane) * 8;
     const bf16_t *xp[MT], *xq[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -76,46 +69,43 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    int s = s0;
-    for (; s + U <= s1; s += U) {
-        bf16x8 wv[U][NT], xv[U][MT], xl[U][MT];
+    if (s0 < s1) {
+        bf16x8 wv[D][NT], xv[D][MT], xl[D][MT];
+        // The ring loads are unconditional: a slot whose k-step lies past the
+        // wavefront's range re-reads its last k-step (a cache hit), so that the
+        // compiler can count outstanding loads exactly.
+        auto load = [&](int j, int st) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) wv[u][nt] = ld16(wp[nt] + (s + u) * 32);
-#pragma unroll
-        for (int u = 0; u < U; ++u)
+            for (int nt = 0; nt < NT; ++nt) wv[j][nt] = ld16(wp[nt] + (size_t)st * 512);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                xv[u][mt] = ld16(xp[mt] + (size_t)(s + u) * 512);
-                xl[u][mt] = ld16(xq[mt] + (size_t)(s + u) * 512);
+                xv[j][mt] = ld16(xp[mt] + (size_t)st * 512);
+                xl[j][mt] = ld16(xq[mt] + (size_t)st * 512);
             }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
+        };
+        auto mma = [&](int j) {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
-                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[u][mt], wv[u][nt], acc[mt][nt], 0, 0, 0);
-                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl[u][mt], wv[u][nt], acc[mt][nt], 0, 0, 0);
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[j][mt], wv[j][nt], acc[mt][nt], 0, 0, 0);
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl[j][mt], wv[j][nt], acc[mt][nt], 0, 0, 0);
                 }
-    }
-    for (; s < s1; ++s) {
-        bf16x8 wv[NT], xv[MT], xl[MT];
+        };
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) wv[nt] = ld16(wp[nt] + s * 32);
+        for (int j = 0; j < D; ++j) load(j, min(s0 + j, s1 - 1));
+        int s = s0;
+        for (; s + D <= s1; s += D) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            xv[mt] = ld16(xp[mt] + (size_t)s * 512);
-            xl[mt] = ld16(xq[mt] + (size_t)s * 512);
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[mt], wv[nt], acc[mt][nt], 0, 0, 0);
-                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl[mt], wv[nt], acc[mt][nt], 0, 0, 0);
+            for (int j = 0; j < D; ++j) {
+                mma(j);
+                load(j, min(s + j + D, s1 - 1));
             }
+        }
+        // fewer than D k-steps remain, already in the ring
+#pragma unroll
+        for (int j = 0; j < D; ++j)
+            if (s + j < s1) mma(j);
     }
 
     // sum the four wavefronts in a fixed order; accumulator layout: lane l holds
@@ -136,28 +126,31 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     }
 
     const int R = a.R;
+    const int tiles_here = min(NT, a.ntiles - tg * NT);
     if (EPI == EPI_SWIGLU) {
-        constexpr int FH = FW / 2;
+        // tile nt, column j < 8: gate of feature 8*(tg*NT+nt)+j; column j+8: its up
         bf16_t *A = (bf16_t *)a.out;
         bf16_t *Al = (bf16_t *)a.out_lo;
-        for (int i = threadIdx.x; i < R * FH; i += 256) {
-            const int r = i / FH, f = i - r * FH;
-            store_operand(A, Al, perm_offset(r, tile * FH + f, a.N), silu_f(red[r][f]) * red[r][FH + f]);
+        const int nf = 8 * tiles_here;
+        for (int i = threadIdx.x; i < R * nf; i += 256) {
+            const int r = i / nf, c = i - r * nf;
+            const int nt = c >> 3, j = c & 7;
+            const float g = red[r][16 * nt + j], u = red[r][16 * nt + 8 + j];
+            store_operand(A, Al, perm_offset(r, 8 * (tg * NT + nt) + j, a.N), silu_f(g) * u);
         }
     } else {
         float *out = (float *)a.out + (size_t)sp * R * a.N;
-        for (int i = threadIdx.x; i < R * FW; i += 256) {
-            const int r = i / FW, c = i - r * FW;
-            out[(size_t)r * a.N + tile * FW + c] = red[r][c];
+        const int nc = 16 * tiles_here;
+        for (int i = threadIdx.x; i < R * nc; i += 256) {
+            const int r = i / nc, c = i - r * nc;
+            out[(size_t)r * a.N + tg * FW + c] = red[r][c];
         }
     }
 }
 
 template <int MT, int NT>
 hipError_t launch_mt_nt(int epi, const SkinnyArgs &a, hipStream_t s) {
-    constexpr int FW = 16 * NT;
-    const int tiles = epi == EPI_SWIGLU ? a.N / (FW / 2) : a.N / FW;
-    dim3 grid(tiles * a.split);
+    dim3 grid(((a.ntiles + NT - 1) / NT) * a.split);
     if (epi == EPI_SWIGLU) hipLaunchKernelGGL((linear_skinny_kernel<MT, NT, EPI_SWIGLU>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((linear_skinny_kernel<MT, NT, EPI_STORE>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
@@ -177,15 +170,22 @@ hipError_t launch_nt(int epi, const SkinnyArgs &a, hipStream_t s) {
 
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s) {
     if (a.R <= 0) return hipSuccess;
-    const int ncols = epi == EPI_SWIGLU ? 2 * a.N : a.N;
-    if (!a.x_lo || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
-    if (a.R > 64 || a.K % 32 != 0 || a.split < 1 || (epi == EPI_SWIGLU && a.split != 1) ||
-        (nt != 1 && nt != 2 && nt != 4 && nt != 8) || ncols % (16 * nt) != 0 || (epi == EPI_SWIGLU && nt < 2))
+    if (!a.x_lo || !a.w || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
+    if (epi != EPI_STORE && epi != EPI_SWIGLU) return hipErrorInvalidValue;
+    const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+    if (a.R > 64 || a.K % 32 != 0 || a.split < 1 || (epi == EPI_SWIGLU && a.split != 1) || vrows % 16 != 0 ||
+        a.ntiles != vrows / 16 || nt < 1 || nt > 8)
         return hipErrorInvalidValue;
-    if (nt == 1) return launch_nt<1>(epi, a, s);
-    if (nt == 2) return launch_nt<2>(epi, a, s);
-    if (nt == 4) return launch_nt<4>(epi, a, s);
-    return launch_nt<8>(epi, a, s);
+    switch (nt) {
+        case 1: return launch_nt<1>(epi, a, s);
+        case 2: return launch_nt<2>(epi, a, s);
+        case 3: return launch_nt<3>(epi, a, s);
+        case 4: return launch_nt<4>(epi, a, s);
+        case 5: return launch_nt<5>(epi, a, s);
+        case 6: return launch_nt<6>(epi, a, s);
+        case 7: return launch_nt<7>(epi, a, s);
+        default: return launch_nt<8>(epi, a, s);
+    }
 }
 
 }  // namespace kvr
