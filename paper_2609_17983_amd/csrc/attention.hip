@@ -275,10 +275,14 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     }
 }
 
-// One block per (combine item, query head of the group, row): merge the split
-// partials of one row in a single pass with running max rescaling (exp2 domain).
+// One block per (combine item, query head of the group, row), one thread per
+// head dimension: merge the split partials of one row with log-sum-exp
+// weights (exp2 domain).  The maximum over the parts is taken first so that
+// every part's loads are independent of the others' (batches of eight loads in
+// flight); the parts are then summed in ascending order.
 __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
                                                                 int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm) {
+    constexpr int B = 8;
     const CombineItem it = items[blockIdx.x];
     const int t = blockIdx.y, i = blockIdx.z;
     if (i >= it.nrows) return;
@@ -286,16 +290,43 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
     const int rows_item = 16 * MT;
     const int j = it.kvh * G + t;
     const int d = threadIdx.x;  // 0..127
-    float M = -INFINITY, L = 0.f, acc = 0.f;
-    for (int q = 0; q < it.nparts; ++q) {
-        const float *p = part + ((size_t)((it.part0 + q) * G + t) * rows_item + i) * PART_ROW;
-        const float mq = p[HD], lq = p[HD + 1], oq = p[d];
-        if (mq == -INFINITY) continue;
-        const float Mn = fmaxf(M, mq);
-        const float a = exp2f(M - Mn), b = exp2f(mq - Mn);
-        acc = acc * a + oq * b;
-        L = L * a + lq * b;
-        M = Mn;
+    const size_t qstride = (size_t)G * rows_item * PART_ROW;
+    const float *base = part + ((size_t)(it.part0 * G + t) * rows_item + i) * PART_ROW;
+    const int np = it.nparts;
+    float M = -INFINITY;
+    int q = 0;
+    for (; q + B <= np; q += B) {
+        float mm[B];
+#pragma unroll
+        for (int u = 0; u < B; ++u) mm[u] = base[(q + u) * qstride + HD];
+#pragma unroll
+        for (int u = 0; u < B; ++u) M = fmaxf(M, mm[u]);
+    }
+    for (; q < np; ++q) M = fmaxf(M, base[q * qstride + HD]);
+    float acc = 0.f, L = 0.f;
+    q = 0;
+    for (; q + B <= np; q += B) {
+        float mm[B], ll[B], oo[B];
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+            const float *p = base + (q + u) * qstride;
+            mm[u] = p[HD];
+            ll[u] = p[HD + 1];
+            oo[u] = p[d];
+        }
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+            const float wq = mm[u] == -INFINITY ? 0.f : exp2f(mm[u] - M);
+            acc += oo[u] * wq;
+            L += ll[u] * wq;
+        }
+    }
+    for (; q < np; ++q) {
+        const float *p = base + q * qstride;
+        const float mq = p[HD];
+        const float wq = mq == -INFINITY ? 0.f : exp2f(mq - M);
+        acc += p[d] * wq;
+        L += p[HD + 1] * wq;
     }
     const int r = it.row0 + i, c = j * HD + d;
     store_operand(O, O_lo, o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c, acc / L);

@@ -174,7 +174,7 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
     if (epi != EPI_STORE && epi != EPI_SWIGLU) return hipErrorInvalidValue;
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.R > 64 || a.K % 32 != 0 || a.split < 1 || (epi == EPI_SWIGLU && a.split != 1) || vrows % 16 != 0 ||
-        a.ntiles != vrows / 16 || nt < 1 || nt > 8)
+        a.ntiles != vrows / 16)
         return hipErrorInvalidValue;
     switch (nt) {
         case 1: return launch_nt<1>(epi, a, s);
@@ -184,7 +184,11 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
         case 5: return launch_nt<5>(epi, a, s);
         case 6: return launch_nt<6>(epi, a, s);
         case 7: return launch_nt<7>(epi, a, s);
-        default: return launch_nt<8>(epi, a, s);
+        case 8: return launch_nt<8>(epi, a, s);
+        case 12: return launch_nt<12>(epi, a, s);
+        case 14: return launch_nt<14>(epi, a, s);
+        case 16: return launch_nt<16>(epi, a, s);
+        default: return hipErrorInvalidValue;
     }
 }
 

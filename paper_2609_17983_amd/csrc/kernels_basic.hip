@@ -50,52 +50,85 @@ __device__ __forceinline__ float block_sum1024(float v, float *red) {
     return t;
 }
 
-// h4 = H[r][4i..4i+3] + the split-K partial tiles part[q][r][4i..] in order.
+// h4 = H[r][4i..4i+3] + the split-K partial tiles part[q][r][4i..] in order
+// (batches of eight independent loads).
 __device__ __forceinline__ float4 add_partials(float4 h, const float *part, int nsplit, int R, int r, int d, int i) {
+    constexpr int B = 8;
     int q = 0;
-    for (; q + 4 <= nsplit; q += 4) {
-        float4 p[4];
+    for (; q + B <= nsplit; q += B) {
+        float4 p[B];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) p[u] = *reinterpret_cast<const float4 *>(part + ((size_t)(q + u) * R + r) * d + 4 * i);
+        for (int u = 0; u < B; ++u) p[u] = *reinterpret_cast<const float4 *>(part + ((size_t)(q + u) * R + r) * d + 4 * i);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) { h.x += p[u].x; h.y += p[u].y; h.z += p[u].z; h.w += p[u].w; }
+        for (int u = 0; u < B; ++u) { h.x += p[u].x; h.y += p[u].y; h.z += p[u].z; h.w += p[u].w; }
     }
-    for (; q < nsplit; ++q) {
-        const float4 p = *reinterpret_cast<const float4 *>(part + ((size_t)q * R + r) * d + 4 * i);
-        h.x += p.x; h.y += p.y; h.z += p.z; h.w += p.w;
+    if (q < nsplit) {
+        float4 p[B];
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+            if (q + u < nsplit) p[u] = *reinterpret_cast<const float4 *>(part + ((size_t)(q + u) * R + r) * d + 4 * i);
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+            if (q + u < nsplit) { h.x += p[u].x; h.y += p[u].y; h.z += p[u].z; h.w += p[u].w; }
     }
     return h;
 }
 
+constexpr int NORM_V = 4;  // float4 per thread of the row kernels: d <= 16384
+
+// Four consecutive outputs (columns c..c+3, c % 4 == 0) of an operand row;
+// they are contiguous in both the row-major and the operand-order layout.
+template <typename T>
+__device__ __forceinline__ void store_operand4(T *hi, T *lo, size_t off, const float (&x)[4]) {
+    if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<float4 *>(hi + off) = make_float4(x[0], x[1], x[2], x[3]);
+    } else {
+        uint32_t h[2], l[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const bf16_t h0 = f32_to_bf16(x[2 * q]), h1 = f32_to_bf16(x[2 * q + 1]);
+            h[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            const bf16_t l0 = f32_to_bf16(x[2 * q] - bf16_to_f32(h0)), l1 = f32_to_bf16(x[2 * q + 1] - bf16_to_f32(h1));
+            l[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        *reinterpret_cast<uint2 *>(hi + off) = make_uint2(h[0], h[1]);
+        if (lo) *reinterpret_cast<uint2 *>(lo + off) = make_uint2(l[0], l[1]);
+    }
+}
+
 // H[r] += sum of the split-K partial tiles (fixed order), then
 // X = H * rsqrt(mean(H^2) + eps) * gain in the operand type (row-major or
-// operand order).  One 1024-thread block per row, four columns per thread
-// per pass (d % 4 == 0).
+// operand order).  One 1024-thread block per row; the row stays in registers
+// between the two passes (four columns per thread per pass, d % 4 == 0).
 template <typename TO, typename TG, bool PERM>
 __global__ __launch_bounds__(1024) void rmsnorm_kernel(float *H, const float *part, int nsplit, int R,
                                                        const TG *gain, int d, float eps, TO *X, TO *X_lo, int ldx) {
     __shared__ float red[16];
     const int r = blockIdx.x;
     float *h = H + (size_t)r * d;
+    float4 v[NORM_V];
     float ss = 0.f;
-    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
-        float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
+#pragma unroll
+    for (int k = 0; k < NORM_V; ++k) {
+        const int i = threadIdx.x + 1024 * k;
+        if (4 * i >= d) break;
+        v[k] = *reinterpret_cast<const float4 *>(h + 4 * i);
         if (nsplit) {
-            v = add_partials(v, part, nsplit, R, r, d, i);
-            *reinterpret_cast<float4 *>(h + 4 * i) = v;
+            v[k] = add_partials(v[k], part, nsplit, R, r, d, i);
+            *reinterpret_cast<float4 *>(h + 4 * i) = v[k];
         }
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
     }
     ss = block_sum1024(ss, red);
     const float inv = rsqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; 4 * i < d; i += 1024) {
-        const float4 v = *reinterpret_cast<const float4 *>(h + 4 * i);
-        const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int c = 4 * i + e;
-            store_operand(X, X_lo, PERM ? perm_offset(r, c, d) : (size_t)r * ldx + c, vv[e] * inv * to_f32(gain[c]));
-        }
+    for (int k = 0; k < NORM_V; ++k) {
+        const int i = threadIdx.x + 1024 * k;
+        if (4 * i >= d) break;
+        const int c = 4 * i;
+        const float x[4] = {v[k].x * inv * to_f32(gain[c]), v[k].y * inv * to_f32(gain[c + 1]),
+                            v[k].z * inv * to_f32(gain[c + 2]), v[k].w * inv * to_f32(gain[c + 3])};
+        store_operand4(X, X_lo, PERM ? perm_offset(r, c, d) : (size_t)r * ldx + c, x);
     }
 }
 
@@ -330,7 +363,7 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
 hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
                           int R, int d, float eps, void *X, void *X_lo, int ldx, bool perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
-    if (d % 4 != 0) return hipErrorInvalidValue;
+    if (d % 4 != 0 || d > 4 * 1024 * NORM_V || (!perm && ldx % 4 != 0)) return hipErrorInvalidValue;
     if (bf16_out && bf16_gain) {
         if (perm)
             hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, true>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
