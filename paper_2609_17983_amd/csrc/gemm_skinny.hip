@@ -35,6 +35,11 @@ __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)
 __device__ __forceinline__ bf16x8 ld16(const bf16_t *p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
 }
+// Weights are read exactly once per pass: stream them with the nontemporal
+// hint so that they do not evict the activations, which every block re-reads.
+__device__ __forceinline__ bf16x8 ld16_stream(const bf16_t *p) {
+    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p)));
+}
 
 template <int MT, int NT, int EPI>
 __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
@@ -76,7 +81,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         // compiler can count outstanding loads exactly.
         auto load = [&](int j, int st) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) wv[j][nt] = ld16(wp[nt] + (size_t)st * 512);
+            for (int nt = 0; nt < NT; ++nt) wv[j][nt] = ld16_stream(wp[nt] + (size_t)st * 512);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 xv[j][mt] = ld16(xp[mt] + (size_t)st * 512);
