@@ -169,13 +169,13 @@ kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_start, int32_t 
 
 /* Per-step GPU time accounting, a tracing aid for benchmarks.  While enabled
  * (it is off after kvr_create), every kernel launch of a prefill or repair
- * pass is followed by a HIP event recorded on the call's stream, tagged with
- * the step of the layer loop it belongs to ("embed", "rmsnorm", "qkv_proj",
- * "rope_scatter", "attention", "attention_combine", "o_proj",
- * "gate_up_swiglu", "down_proj", "final_norm").  The time of a launch is the
- * elapsed time from the previous event of its pass to its own event (kernel
- * duration plus the gap before it).  Enabling adds one event per launch.
- * Errors: KVR_E_ARG (NULL context). */
+ * pass is made with a pair of HIP events that the dispatch records at the
+ * start and at the end of the kernel's execution (hipExtLaunchKernel), tagged
+ * with the step of the layer loop it belongs to ("embed", "rmsnorm",
+ * "qkv_proj", "rope_scatter", "attention", "attention_combine", "o_proj",
+ * "gate_up_swiglu", "down_proj", "final_norm").  The time of a launch is its
+ * execution time; the dispatch gaps between kernels are not counted, so the
+ * step times sum to less than the pass.  Errors: KVR_E_ARG (NULL context). */
 kvr_status kvr_profile_enable(kvr_ctx *ctx, int32_t enable);
 
 /* Wait for the recorded events, add their times to per-step totals and report

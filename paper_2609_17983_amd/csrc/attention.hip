@@ -347,10 +347,10 @@ hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowI
     const int MT = attention_row_tiles(Hq, Hkv);
     const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
     if (ppw == 1)
-        hipLaunchKernelGGL(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+        kvr_launch(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
                            layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
     else if (ppw == 2)
-        hipLaunchKernelGGL(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+        kvr_launch(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
                            layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
     else
         return hipErrorInvalidValue;
@@ -361,7 +361,7 @@ hipError_t launch_attention_combine(const CombineItem *items, int n_items, const
                                     bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     const int MT = attention_row_tiles(Hq, Hkv);
-    hipLaunchKernelGGL(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
+    kvr_launch(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
                        Hkv, MT, O, O_lo, (int)o_perm);
     return hipGetLastError();
 }

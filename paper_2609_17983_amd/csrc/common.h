@@ -1,6 +1,7 @@
 // Internal declarations shared by the library's HIP sources.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -128,7 +129,26 @@ struct SkinnyArgs {
     int32_t split;
 };
 
-// ---- launchers (each enqueues on `stream`; return hipSuccess or the launch error)
+// ---- kernel launch with optional execution timing
+//
+// While launch_timer() holds events (the context's step profiler arms it
+// before a launcher call), the next launch records them at the start and the
+// end of the kernel's execution (hipExtLaunchKernel), which excludes the
+// dispatch gap in front of the kernel; the launch disarms the timer.
+struct LaunchTimer {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchTimer &launch_timer();
+
+template <typename... KArgs, typename... Args>
+inline void kvr_launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t s,
+                       Args... args) {
+    LaunchTimer &t = launch_timer();
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, t.start, t.stop, 0, static_cast<KArgs>(args)...);
+    t.start = t.stop = nullptr;
+}
+
+// ---- launchers (each enqueues one kernel on `stream`; return hipSuccess or the launch error)
 
 hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int R, const void *embed,
                         int d, int vocab, float *H, hipStream_t s);

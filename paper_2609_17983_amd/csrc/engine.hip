@@ -26,6 +26,11 @@ namespace kvr {
 static thread_local std::string g_error;
 void set_global_error(const char *msg) { g_error = msg; }
 
+LaunchTimer &launch_timer() {
+    static thread_local LaunchTimer t;
+    return t;
+}
+
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -65,7 +70,8 @@ struct kvr_ctx {
     // per-step event profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_pool;
-    std::vector<std::pair<int, hipEvent_t>> ev_marks;  // (step ending at this event, or -1), event
+    struct Timed { int step; hipEvent_t start, stop; };
+    std::vector<Timed> ev_marks;  // launches timed since the last read
     double step_ms[16] = {};
     long long step_n[16] = {};
 
@@ -236,20 +242,36 @@ hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N,
     return launch_linear_skinny(epi, a, p.nt, s);
 }
 
-// Profiling mark: the event ends the launch(es) of `step` enqueued since the
-// previous mark (-1 opens a pass).
-hipError_t mark(kvr_ctx *c, int step, hipStream_t s) {
-    if (!c->profiling) return hipSuccess;
-    hipEvent_t ev;
+// Step profiler: arm() hands two events to the next kernel launch, which
+// records them around its execution; disarm() files them under `step` (or
+// returns them when the launcher enqueued nothing).
+hipError_t take_event(kvr_ctx *c, hipEvent_t *ev) {
     if (!c->ev_pool.empty()) {
-        ev = c->ev_pool.back();
+        *ev = c->ev_pool.back();
         c->ev_pool.pop_back();
-    } else {
-        hipError_t e = hipEventCreate(&ev);
-        if (e != hipSuccess) return e;
+        return hipSuccess;
     }
-    c->ev_marks.push_back({step, ev});
-    return hipEventRecord(ev, s);
+    return hipEventCreate(ev);
+}
+
+hipError_t arm(kvr_ctx *c) {
+    if (!c->profiling) return hipSuccess;
+    LaunchTimer &t = launch_timer();
+    hipError_t e = take_event(c, &t.start);
+    if (e == hipSuccess) e = take_event(c, &t.stop);
+    return e;
+}
+
+void disarm(kvr_ctx *c, int step, hipEvent_t start, hipEvent_t stop) {
+    if (!c->profiling || !start) return;
+    LaunchTimer &t = launch_timer();
+    if (t.start == nullptr) {
+        c->ev_marks.push_back({step, start, stop});  // consumed by a launch
+    } else {
+        c->ev_pool.push_back(start);
+        c->ev_pool.push_back(stop);
+        t.start = t.stop = nullptr;
+    }
 }
 
 // Upload the tables of a pass and enqueue its kernels.
@@ -298,14 +320,15 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
         p_gu = plan_skinny(2 * F / 16, D, true, "KVR_NT_GATEUP", nullptr);
         p_down = plan_skinny(D / 16, F, false, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
     }
-#define KVR_CHECK(expr, what, step)                                  \
-    do {                                                             \
-        hipError_t err_ = (expr);                                    \
-        if (err_ == hipSuccess) err_ = mark(c, step, s);             \
-        if (err_ != hipSuccess) return hip_fail(c, err_, what);      \
+#define KVR_CHECK(expr, what, step)                                                \
+    do {                                                                           \
+        hipError_t err_ = arm(c);                                                  \
+        const LaunchTimer armed_ = launch_timer();                                 \
+        if (err_ == hipSuccess) err_ = (expr);                                     \
+        disarm(c, step, armed_.start, armed_.stop);                                \
+        if (err_ != hipSuccess) return hip_fail(c, err_, what);                    \
     } while (0)
 
-    KVR_CHECK(hipSuccess, "profiling mark", -1);
     KVR_CHECK(launch_embed(bf, rows, docs, R, c->embed, D, d.vocab, c->H, s), "embed", ST_EMBED);
     int resid_split = 0;  // partial tiles in P still to be added to H
     for (int l = 0; l < d.n_layers; ++l) {
@@ -547,7 +570,10 @@ void kvr_destroy(kvr_ctx *c) {
         DeviceGuard g(c->device);
         (void)hipDeviceSynchronize();
         if (c->stage_ev) (void)hipEventDestroy(c->stage_ev);
-        for (auto &m : c->ev_marks) (void)hipEventDestroy(m.second);
+        for (auto &m : c->ev_marks) {
+            (void)hipEventDestroy(m.start);
+            (void)hipEventDestroy(m.stop);
+        }
         for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
         if (c->h_stage) (void)hipHostFree(c->h_stage);
         if (c->ws) (void)hipFree(c->ws);
@@ -590,18 +616,19 @@ kvr_status kvr_profile_read(kvr_ctx *c, int32_t capacity, const char **names, do
         return fail(c, KVR_E_ARG, "kvr_profile_read: bad arguments");
     DeviceGuard g(c->device);
     if (!c->ev_marks.empty()) {
-        hipError_t e = hipEventSynchronize(c->ev_marks.back().second);
+        hipError_t e = hipEventSynchronize(c->ev_marks.back().stop);
         if (e != hipSuccess) return hip_fail(c, e, "kvr_profile_read");
-        for (size_t i = 1; i < c->ev_marks.size(); ++i) {
-            const int st = c->ev_marks[i].first;
-            if (st < 0) continue;
+        for (const auto &m : c->ev_marks) {
             float ms = 0.f;
-            e = hipEventElapsedTime(&ms, c->ev_marks[i - 1].second, c->ev_marks[i].second);
+            e = hipEventElapsedTime(&ms, m.start, m.stop);
             if (e != hipSuccess) return hip_fail(c, e, "kvr_profile_read: hipEventElapsedTime");
-            c->step_ms[st] += ms;
-            c->step_n[st] += 1;
+            c->step_ms[m.step] += ms;
+            c->step_n[m.step] += 1;
         }
-        for (auto &m : c->ev_marks) c->ev_pool.push_back(m.second);
+        for (const auto &m : c->ev_marks) {
+            c->ev_pool.push_back(m.start);
+            c->ev_pool.push_back(m.stop);
+        }
         c->ev_marks.clear();
     }
     *n_steps = ST_COUNT;

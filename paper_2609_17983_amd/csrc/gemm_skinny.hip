@@ -156,8 +156,8 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
 template <int MT, int NT>
 hipError_t launch_mt_nt(int epi, const SkinnyArgs &a, hipStream_t s) {
     dim3 grid(((a.ntiles + NT - 1) / NT) * a.split);
-    if (epi == EPI_SWIGLU) hipLaunchKernelGGL((linear_skinny_kernel<MT, NT, EPI_SWIGLU>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((linear_skinny_kernel<MT, NT, EPI_STORE>), grid, dim3(256), 0, s, a);
+    if (epi == EPI_SWIGLU) kvr_launch((linear_skinny_kernel<MT, NT, EPI_SWIGLU>), grid, dim3(256), 0, s, a);
+    else kvr_launch((linear_skinny_kernel<MT, NT, EPI_STORE>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

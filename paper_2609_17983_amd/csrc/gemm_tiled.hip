@@ -152,9 +152,9 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.K % BK != 0 || a.ldx % 8 != 0 || vrows % 16 != 0) return hipErrorInvalidValue;
     dim3 grid((vrows + BN - 1) / BN, (a.R + BM - 1) / BM);
-    if (epi == EPI_STORE) hipLaunchKernelGGL(linear_tiled_kernel<EPI_STORE>, grid, dim3(256), 0, s, a);
-    else if (epi == EPI_RESID) hipLaunchKernelGGL(linear_tiled_kernel<EPI_RESID>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(linear_tiled_kernel<EPI_SWIGLU>, grid, dim3(256), 0, s, a);
+    if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE>, grid, dim3(256), 0, s, a);
+    else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID>, grid, dim3(256), 0, s, a);
+    else kvr_launch(linear_tiled_kernel<EPI_SWIGLU>, grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

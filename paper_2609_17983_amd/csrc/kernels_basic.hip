@@ -352,10 +352,10 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
                         int vocab, float *H, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (bf16)
-        hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(R), dim3(256), 0, s, rows, docs, (const bf16_t *)embed, d, vocab,
+        kvr_launch(embed_kernel<bf16_t>, dim3(R), dim3(256), 0, s, rows, docs, (const bf16_t *)embed, d, vocab,
                            H);
     else
-        hipLaunchKernelGGL(embed_kernel<float>, dim3(R), dim3(256), 0, s, rows, docs, (const float *)embed, d, vocab,
+        kvr_launch(embed_kernel<float>, dim3(R), dim3(256), 0, s, rows, docs, (const float *)embed, d, vocab,
                            H);
     return hipGetLastError();
 }
@@ -366,13 +366,13 @@ hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *
     if (d % 4 != 0 || d > 4 * 1024 * NORM_V || (!perm && ldx % 4 != 0)) return hipErrorInvalidValue;
     if (bf16_out && bf16_gain) {
         if (perm)
-            hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, true>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+            kvr_launch((rmsnorm_kernel<bf16_t, bf16_t, true>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
                                (const bf16_t *)gain, d, eps, (bf16_t *)X, (bf16_t *)X_lo, ldx);
         else
-            hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, bf16_t, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+            kvr_launch((rmsnorm_kernel<bf16_t, bf16_t, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
                                (const bf16_t *)gain, d, eps, (bf16_t *)X, (bf16_t *)X_lo, ldx);
     } else if (!bf16_out && !bf16_gain && !perm) {
-        hipLaunchKernelGGL((rmsnorm_kernel<float, float, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+        kvr_launch((rmsnorm_kernel<float, float, false>), dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
                            (const float *)gain, d, eps, (float *)X, (float *)nullptr, ldx);
     } else {
         return hipErrorInvalidValue;
@@ -385,10 +385,10 @@ hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int ns
     if (R <= 0) return hipSuccess;
     if (d % 4 != 0) return hipErrorInvalidValue;
     if (bf16_gain)
-        hipLaunchKernelGGL(final_norm_kernel<bf16_t>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+        kvr_launch(final_norm_kernel<bf16_t>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
                            (const bf16_t *)gain, rows, docs, d, eps);
     else
-        hipLaunchKernelGGL(final_norm_kernel<float>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
+        kvr_launch(final_norm_kernel<float>, dim3(R), dim3(1024), 0, s, H, part, nsplit, R,
                            (const float *)gain, rows, docs, d, eps);
     return hipGetLastError();
 }
@@ -401,11 +401,11 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
     const size_t lds = (size_t)(Hq + 2 * Hkv) * hd * sizeof(float);
     if (lds > 160 * 1024 || ((Hq + 2 * Hkv) * hd) % 4 != 0) return hipErrorInvalidValue;
     if (bf16)
-        hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
+        kvr_launch(rope_scatter_kernel<bf16_t>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
                            (const bf16_t *)bq, (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd,
                            rope_cos, rope_sin, (bf16_t *)Q, (bf16_t *)Q_lo);
     else
-        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
+        kvr_launch(rope_scatter_kernel<float>, dim3(R), dim3(1024), lds, s, qkv, nsplit, R,
                            (const float *)bq, (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd,
                            rope_cos, rope_sin, (float *)Q, (float *)nullptr);
     return hipGetLastError();
@@ -416,10 +416,10 @@ hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, c
                                    bool o_perm, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (bf16)
-        hipLaunchKernelGGL(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q,
+        kvr_launch(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q,
                            (const bf16_t *)Q_lo, rows, docs, layer, Hq, Hkv, hd, (bf16_t *)O, (bf16_t *)O_lo, (int)o_perm);
     else if (!o_perm)
-        hipLaunchKernelGGL(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q,
+        kvr_launch(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q,
                            (const float *)nullptr, rows, docs, layer, Hq, Hkv, hd, (float *)O, (float *)nullptr, 0);
     else
         return hipErrorInvalidValue;
@@ -430,7 +430,7 @@ hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStre
     if (a.R <= 0) return hipSuccess;
     const int cols_per_block = epi == EPI_SWIGLU ? 32 : 64;
     dim3 grid((a.N + cols_per_block - 1) / cols_per_block, (a.R + 63) / 64);
-#define KVR_LS(T, E) hipLaunchKernelGGL((linear_simple_kernel<T, E>), grid, dim3(256), 0, s, a)
+#define KVR_LS(T, E) kvr_launch((linear_simple_kernel<T, E>), grid, dim3(256), 0, s, a)
     if (bf16) {
         if (epi == EPI_STORE) KVR_LS(bf16_t, EPI_STORE);
         else if (epi == EPI_RESID) KVR_LS(bf16_t, EPI_RESID);

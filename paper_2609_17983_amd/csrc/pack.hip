@@ -56,7 +56,7 @@ hipError_t launch_pack_weight(const void *w0, const void *w1, const void *w2, in
     if (V <= 0 || V % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
     const size_t chunks = (size_t)V * K / 8;
     const int grid = (int)std::min<size_t>((chunks + 255) / 256, 65536);
-    hipLaunchKernelGGL(pack_weight_kernel, dim3(grid), dim3(256), 0, s, (const bf16_t *)w0, (const bf16_t *)w1,
+    kvr_launch(pack_weight_kernel, dim3(grid), dim3(256), 0, s, (const bf16_t *)w0, (const bf16_t *)w1,
                        (const bf16_t *)w2, e0, e1, interleave ? 1 : 0, V, K, (bf16_t *)dst);
     return hipGetLastError();
 }
