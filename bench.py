@@ -26,6 +26,7 @@ import sys
 import time
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 WORKLOADS = {
     "llama8b-k32": dict(shape="llama3-8b", n=5000, span=16, K=32, policy="edit_local", lo=1000, hi=4000),
@@ -37,6 +38,9 @@ WORKLOADS = {
     "qwen7b-random-k512": dict(shape="qwen2.5-7b", n=5000, span=16, K=512, policy="random", lo=1000, hi=4000),
     "mistral7b-end": dict(shape="mistral-7b", n=5000, span=16, K=32, policy="edit_local", lo=4900, hi=4900),
     "mistral7b-start": dict(shape="mistral-7b", n=5000, span=16, K=32, policy="edit_local", lo=200, hi=200),
+    # 64 documents of 2000-8000 tokens, one 16-token edit each at 20-80 % of the
+    # document, EditLocal K=32, repaired in one call (3072 rows)
+    "llama8b-batch64": dict(shape="llama3-8b", docs=64, n_lo=2000, n_hi=8000, span=16, K=32, policy="edit_local"),
 }
 
 
@@ -46,6 +50,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b-k32", choices=sorted(WORKLOADS))
+    ap.add_argument("--seeds", type=int, default=5,
+                    help="edit placements (seeds 0..S-1) timed for the per-seed report; value is seed 0's")
     ap.add_argument("--prefill-steps", type=int, default=5)
     ap.add_argument("--cpu-layers", type=int, default=32,
                     help="layers of the repair the CPU oracle runs for its bounded sample")
@@ -59,15 +65,44 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def repair_bytes(shape, rows, max_pos, n_docs_maxpos=None):
-    """Algorithmic HBM bytes of one repair: every weight once, the KV rows
-    [0, max P] of each kv head once, the fresh K/V writes, the embedding rows."""
+def plan_docs(wl, kvr, synth, label):
+    """(n, edit start, A) of every document of the workload for edit seed `label`."""
+    span, K = wl["span"], wl["K"]
+    policy = kvr.KVR_EDIT_LOCAL if wl["policy"] == "edit_local" else kvr.KVR_RANDOM
+    if "docs" not in wl:
+        n = wl["n"]
+        e = synth.edit_position(wl["lo"], wl["hi"], label=label)
+        return [(n, e, kvr.kvr_select(policy, n, e, e + span, K, label))]
+    out = []
+    for i, n in enumerate(synth.doc_lengths(wl["docs"], wl["n_lo"], wl["n_hi"])):
+        e = synth.edit_position(int(0.2 * n), int(0.8 * n) - span, label=1000 * label + i)
+        out.append((n, e, kvr.kvr_select(policy, n, e, e + span, K, label + i)))
+    return out
+
+
+def repair_bytes(shape, plans, span):
+    """Algorithmic HBM bytes of one repair call: every weight once, per document
+    the KV rows [0, max P] of each kv head once and the fresh K/V writes, and
+    the embedding rows."""
     es = 2
-    w = shape.n_layers * shape.layer_params() * es + shape.d_model * es
-    kv_read = (max_pos + 1) * shape.kv_bytes_per_pos(es)
-    kv_write = rows * shape.kv_bytes_per_pos(es)
-    emb = rows * shape.d_model * es
-    return w + kv_read + kv_write + emb
+    b = shape.n_layers * shape.layer_params() * es + shape.d_model * es
+    for n, e, A in plans:
+        R = span + len(A)
+        max_pos = max([e + span - 1] + list(A))
+        b += (max_pos + 1) * shape.kv_bytes_per_pos(es) + R * shape.kv_bytes_per_pos(es) + R * shape.d_model * es
+    return b
+
+
+def repair_flops(shape, plans, span):
+    """Algorithmic flops of one repair call: 2 per weight element per row, and
+    per layer and row at position p: 4 * H_q * head_dim * (p + 1) of attention."""
+    mat = shape.layer_params() - 2 * shape.d_model - (shape.q_dim + 2 * shape.kv_dim if shape.qkv_bias else 0)
+    f = 0
+    for n, e, A in plans:
+        P = list(range(e, e + span)) + list(A)
+        f += 2 * len(P) * shape.n_layers * mat
+        f += shape.n_layers * 4 * shape.n_heads * shape.head_dim * sum(p + 1 for p in P)
+    return f
 
 
 def main():
@@ -85,16 +120,21 @@ def main():
 
     wl = WORKLOADS[args.workload]
     shape = synth.SHAPES[wl["shape"]]
-    n, span, K = wl["n"], wl["span"], wl["K"]
-    e = synth.edit_position(wl["lo"], wl["hi"])
-    policy = kvr.KVR_EDIT_LOCAL if wl["policy"] == "edit_local" else kvr.KVR_RANDOM
-    A = kvr.kvr_select(policy, n, e, e + span, K, 0)
-    R = span + len(A)
-    max_pos = max([e + span - 1] + A)
+    span, K = wl["span"], wl["K"]
+    batched = "docs" in wl
+    plans = plan_docs(wl, kvr, synth, 0)
+    R = sum(span + len(A) for _, _, A in plans)
+    n_max = max(n for n, _, _ in plans)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
+    L = shape.n_layers
+    if batched:
+        log(f"workload {args.workload}: {shape.name}, {len(plans)} docs of {min(n for n, _, _ in plans)}-{n_max} "
+            f"tokens, {wl['policy']} K={K} -> {R} rows")
+    else:
+        n, e, A = plans[0]
+        log(f"workload {args.workload}: {shape.name}, n={n}, edit [{e},{e + span}), {wl['policy']} K={K} -> {R} rows")
 
-    log(f"workload {args.workload}: {shape.name}, n={n}, edit [{e},{e + span}), {wl['policy']} K={K} -> {R} rows")
     if args.calibrate_copy:
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev)
         dst = torch.empty_like(src)
@@ -103,34 +143,47 @@ def main():
         log("calibration copy: 1 GiB read + 1 GiB written")
         del src, dst
     w = synth.make_weights(shape, dtype=torch.bfloat16, device="cuda")
-    dims = kvr.dims_for(shape, kvr.KVR_BF16, max_ctx=n, max_rows=max(R, 64))
-    ws = kvr.weights_struct(w)
-    ctx = kvr.kvr_create(dims, ws)
-    toks = synth.make_tokens(n, shape.vocab).to(dev)
-    new = synth.apply_edit(toks, e, span, shape.vocab)
-    cache = torch.empty((shape.n_layers, 2, shape.n_kv_heads, n, shape.head_dim), dtype=torch.bfloat16, device=dev)
-    kvr.kvr_prefill(ctx, toks.data_ptr(), n, n, cache.data_ptr(), None, stream.cuda_stream)  # stale K(C)
-    hidden = torch.empty((R, shape.d_model), dtype=torch.float32, device=dev)
-    doc = kvr.make_doc(cache.data_ptr(), n, n, new.data_ptr(), e, e + span, A, hidden.data_ptr())
+    dims = kvr.dims_for(shape, kvr.KVR_BF16, max_ctx=n_max, max_rows=max(R, 64))
+    ctx = kvr.kvr_create(dims, kvr.weights_struct(w))
+
+    # stale caches K(C) by the engine's own prefill, then the edited ids C'
+    caches, olds, hiddens = [], [], []
+    for i, (n, e, A) in enumerate(plans):
+        toks = synth.make_tokens(n, shape.vocab, seed=synth.SEED_TOKENS + i).to(dev)
+        cache = torch.empty((L, 2, shape.n_kv_heads, n, shape.head_dim), dtype=torch.bfloat16, device=dev)
+        kvr.kvr_prefill(ctx, toks.data_ptr(), n, n, cache.data_ptr(), None, stream.cuda_stream)
+        caches.append(cache)
+        olds.append(toks)
+        hiddens.append(torch.empty((span + len(A), shape.d_model), dtype=torch.float32, device=dev))
     torch.cuda.synchronize()
+
+    def make_docs(plans_s, label):
+        docs, news = [], []
+        for i, (n, e, A) in enumerate(plans_s):
+            new = synth.apply_edit(olds[i], e, span, shape.vocab, label=1000 * label + i)
+            news.append(new)
+            docs.append(kvr.make_doc(caches[i].data_ptr(), n, n, new.data_ptr(), e, e + span, A,
+                                     hiddens[i].data_ptr() if len(A) + span == hiddens[i].shape[0] else None))
+        return docs, news
+
+    def timed(docs, steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for i in range(steps):
+            kvr.kvr_repair(ctx, docs, stream.cuda_stream)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)], ev[0].elapsed_time(ev[-1]) / steps
 
     # ---- repair: W warmup, then K timed steps (HIP events on the stream the
     # kernels run on)
+    docs, news = make_docs(plans, 0)
     for _ in range(args.warmup):
-        kvr.kvr_repair(ctx, [doc], stream.cuda_stream)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
+        kvr.kvr_repair(ctx, docs, stream.cuda_stream)
     t_wall = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        kvr.kvr_repair(ctx, [doc], stream.cuda_stream)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
+    step_ms, ms = timed(docs, args.steps)
     wall_ms = (time.perf_counter() - t_wall) * 1e3
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
-    total_ms = ev[0].elapsed_time(ev[-1])
-    ms = total_ms / args.steps
     log(f"repair: mean {ms:.3f} ms, median {statistics.median(step_ms):.3f}, min {min(step_ms):.3f} "
         f"(wall {wall_ms / args.steps:.3f} ms/step)")
 
@@ -141,61 +194,99 @@ def main():
     # slows the launches down, so this loop is kept apart from the timed one.
     kvr.kvr_profile_enable(ctx, True)
     kvr.kvr_profile_read(ctx)
-    ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ev2[0].record(stream)
-    for i in range(args.steps):
-        kvr.kvr_repair(ctx, [doc], stream.cuda_stream)
-    ev2[1].record(stream)
-    torch.cuda.synchronize()
+    _, profiled_ms = timed(docs, args.steps)
     prof = kvr.kvr_profile_read(ctx)
     kvr.kvr_profile_enable(ctx, False)
-    profiled_ms = ev2[0].elapsed_time(ev2[1]) / args.steps
     log(f"repair with the step profiler on: {profiled_ms:.3f} ms")
 
-    # ---- same-engine full re-prefill of C'
-    pcache = torch.empty_like(cache)
-    for _ in range(1):
-        kvr.kvr_prefill(ctx, new.data_ptr(), n, n, pcache.data_ptr(), None, stream.cuda_stream)
+    # ---- the other edit placements (single-document workloads): same protocol
+    per_seed = [round(ms, 4)]
+    seed_edits = [plans[0][1]] if not batched else []
+    if not batched:
+        for sd in range(1, args.seeds):
+            ps = plan_docs(wl, kvr, synth, sd)
+            d_s, _ = make_docs(ps, sd)
+            for _ in range(args.warmup):
+                kvr.kvr_repair(ctx, d_s, stream.cuda_stream)
+            per_seed.append(round(timed(d_s, args.steps)[1], 4))
+            seed_edits.append(ps[0][1])
+        log(f"per edit seed ms: {per_seed} (edits at {seed_edits}); median {statistics.median(per_seed):.3f}")
+        docs, news = make_docs(plans, 0)  # restore seed 0's edited ids for the prefill baseline
+
+    # ---- same-engine full re-prefill of every C' (one scratch cache, reused)
+    pcache = torch.empty((L, 2, shape.n_kv_heads, n_max, shape.head_dim), dtype=torch.bfloat16, device=dev)
+    psteps = 1 if batched else args.prefill_steps
+
+    def prefill_all():
+        for i, (n, e, A) in enumerate(plans):
+            kvr.kvr_prefill(ctx, news[i].data_ptr(), n, n_max, pcache.data_ptr(), None, stream.cuda_stream)
+
+    prefill_all()
     torch.cuda.synchronize()
-    pev = [torch.cuda.Event(enable_timing=True) for _ in range(args.prefill_steps + 1)]
+    pev = [torch.cuda.Event(enable_timing=True) for _ in range(psteps + 1)]
     pev[0].record(stream)
-    for i in range(args.prefill_steps):
-        kvr.kvr_prefill(ctx, new.data_ptr(), n, n, pcache.data_ptr(), None, stream.cuda_stream)
+    for i in range(psteps):
+        prefill_all()
         pev[i + 1].record(stream)
     torch.cuda.synchronize()
-    pre_ms = [pev[i].elapsed_time(pev[i + 1]) for i in range(args.prefill_steps)]
-    prefill_ms = statistics.median(pre_ms)
-    log(f"prefill: median {prefill_ms:.2f} ms")
+    prefill_ms = statistics.median([pev[i].elapsed_time(pev[i + 1]) for i in range(psteps)])
+    log(f"prefill of every edited context: median {prefill_ms:.2f} ms")
     del pcache
 
-    L = shape.n_layers
     steps_ms = {k: round(v[0] / args.steps, 4) for k, v in prof.items() if v[1]}
     gu_ms, gu_n = prof["gate_up_swiglu"]
     kern_ms = gu_ms / gu_n
-    kern_bytes = 2 * shape.d_ffn * shape.d_model * 2 + R * shape.d_model * 2 + R * shape.d_ffn * 2
-    kern_gbs = kern_bytes / (kern_ms * 1e-3) / 1e9
     log(f"kernel execution ms per repair by step: {steps_ms} (sum {sum(steps_ms.values()):.3f})")
-    log(f"gate/up+SwiGLU kernel: {kern_ms * 1e3:.1f} us/launch, {kern_gbs:.0f} GB/s")
-
-    traffic = None
-    # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE counter passes, valid
-    # only while the kernel source is the one the counters were taken on
-    tfile = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                         "gateup_swiglu_llama8b_r48_traffic.md")
-    if wl["shape"] == "llama3-8b" and R == 48 and os.path.exists(tfile):
-        with open(tfile) as f:
-            kv = dict(l.split(": ", 1) for l in f.read().splitlines() if l.startswith(("hbm_bytes", "kernel_source")))
-        if kv.get("kernel_source_sha") == _kernel_sha():
-            traffic = int(kv["hbm_bytes_per_launch"])
+    d_, F_ = shape.d_model, shape.d_ffn
+    if R <= 64:
+        kern_bytes = 2 * F_ * d_ * 2 + R * d_ * 2 + R * F_ * 2
+        achieved = kern_bytes / (kern_ms * 1e-3) / 1e9
+        traffic = None
+        # HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE counter passes,
+        # valid only while the kernel source is the one the counters were taken on
+        tfile = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                             "gateup_swiglu_llama8b_r48_traffic.md")
+        if wl["shape"] == "llama3-8b" and R == 48 and os.path.exists(tfile):
+            with open(tfile) as f:
+                kv = dict(l.split(": ", 1) for l in f.read().splitlines() if l.startswith(("hbm_bytes", "kernel_source")))
+            if kv.get("kernel_source_sha") == _kernel_sha():
+                traffic = int(kv["hbm_bytes_per_launch"])
+        roof = {"kernel": "gate/up projection + SwiGLU (linear_skinny_kernel, SWIGLU epilogue)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": kern_bytes, "avg_launch_us": round(kern_ms * 1e3, 2)}
+    else:
+        kern_flops = 2 * R * 2 * F_ * d_
+        achieved = kern_flops / (kern_ms * 1e-3) / 1e12
+        roof = {"kernel": "gate/up projection + SwiGLU (linear_tiled_kernel, SWIGLU epilogue)", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "algorithmic_flops_per_launch": kern_flops, "avg_launch_us": round(kern_ms * 1e3, 2),
+                "issued_mfma_frac": round(2 * achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+    log(f"gate/up+SwiGLU kernel: {kern_ms * 1e3:.1f} us/launch, {roof['achieved']} {roof['unit']}")
 
     # ---- fp64 CPU oracle on a bounded sample of the same repair
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(shape, w, n, e, span, A, min(args.cpu_layers, L), torch)
+        n0, e0, A0 = plans[0]
+        cpu = cpu_baseline(shape, w, n0, e0, span, A0, min(args.cpu_layers, L), len(plans), torch)
 
-    rbytes = repair_bytes(shape, R, max_pos)
+    rbytes = repair_bytes(shape, plans, span)
+    rflops = repair_flops(shape, plans, span)
+    if batched:
+        cfg = {"workload": f"{shape.name}-shaped batched repair: {len(plans)} documents of "
+                           f"{wl['n_lo']}-{wl['n_hi']} tokens, one {span}-token edit each, {wl['policy']} K={K}",
+               "docs": len(plans), "rows": R, "K": K, "policy": wl["policy"],
+               "n_ctx_total": sum(n for n, _, _ in plans)}
+        metric = "ms per batched repair call (64 docs, 8B shape); MFMA TFLOP/s; speedup vs re-prefill of every doc"
+    else:
+        n, e, A = plans[0]
+        cfg = {"workload": f"{shape.name}-shaped repair, n={n}, {span}-token edit at {e}, {wl['policy']} K={K}, "
+                           f"batch 1", "n_ctx": n, "edit": [e, e + span], "K": K, "rows": R,
+               "policy": wl["policy"], "batch": 1}
+        metric = "ms per repair @5k ctx K=32 (8B shape), HBM GB/s; speedup vs full re-prefill"
     out = {
-        "metric": "ms per repair @5k ctx K=32 (8B shape), HBM GB/s; speedup vs full re-prefill",
+        "metric": metric,
         "value": round(ms, 4),
         "unit": "ms/repair",
         "n_gpus": 1,
@@ -207,27 +298,29 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic: random-init N(0,0.02) bf16 weights, uniform token ids, seeded edit",
-        "config": {"workload": f"{shape.name}-shaped repair, n={n}, {span}-token edit at {e}, "
-                               f"{wl['policy']} K={K}, batch 1",
-                   "n_ctx": n, "edit": [e, e + span], "K": K, "rows": R, "policy": wl["policy"], "batch": 1},
+        "config": cfg,
         "median_ms": round(statistics.median(step_ms), 4),
         "min_ms": round(min(step_ms), 4),
         "hbm_gb_s": round(rbytes / (ms * 1e-3) / 1e9, 1),
         "hbm_frac": round(rbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "algorithmic_bytes_per_repair": rbytes,
+        "mfma_tflops": round(rflops / (ms * 1e-3) / 1e12, 2),
+        "mfma_frac": round(rflops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "algorithmic_flops_per_repair": rflops,
         "recomputed_tokens_per_s": round(R / (ms * 1e-3), 1),
         "token_layers_per_s": round(R * L / (ms * 1e-3), 1),
         "prefill_ms": round(prefill_ms, 3),
         "speedup_vs_prefill": round(prefill_ms / ms, 2),
-        "token_layer_proxy_speedup": round(n / R, 2),
+        "token_layer_proxy_speedup": round(sum(n for n, _, _ in plans) / R, 2),
         "kernel_ms_per_repair_by_step": steps_ms,
         "profiled_loop_ms": round(profiled_ms, 4),
-        "roofline": {"kernel": "gate/up projection + SwiGLU (linear_skinny_kernel, SWIGLU epilogue)",
-                     "bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(kern_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": kern_bytes, "avg_launch_us": round(kern_ms * 1e3, 2)},
+        "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if not batched:
+        out["per_seed_ms"] = per_seed
+        out["per_seed_edits"] = seed_edits
+        out["median_over_seeds_ms"] = round(statistics.median(per_seed), 4)
     print(json.dumps(out), flush=True)
     kvr.kvr_destroy(ctx)
 
@@ -239,10 +332,10 @@ def _kernel_sha():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def cpu_baseline(shape, w, n, e, span, A, layers, torch):
-    """The fp64 oracle repairing the first `layers` layers of the same repair
-    (same weights, a synthetic stale cache of the same shape), scaled to all
-    layers."""
+def cpu_baseline(shape, w, n, e, span, A, layers, n_docs, torch):
+    """The fp64 oracle repairing the first `layers` layers of the (first
+    document's) repair (same weights, a synthetic stale cache of the same
+    shape), scaled to all layers and documents."""
     import numpy as np
     import synth
     from oracle import decoder as od
@@ -269,12 +362,13 @@ def cpu_baseline(shape, w, n, e, span, A, layers, torch):
     t0 = time.perf_counter()
     od.repair(shape, HostWeights(), stale, toks, e, e + span, A, n_layers=layers)
     dt = time.perf_counter() - t0
-    per_repair_ms = dt * 1e3 * shape.n_layers / layers
+    per_repair_ms = dt * 1e3 * shape.n_layers / layers * n_docs
     log(f"cpu baseline: {dt:.2f} s for {layers} layers -> {per_repair_ms:.0f} ms per repair")
     return {"value": round(per_repair_ms, 1), "unit": "ms/repair", "cores": threads, "kind": "oracle",
             "host_cpus": os.cpu_count(),
             "sample": f"fp64 numpy oracle repair of layers 0-{layers - 1} of {shape.n_layers} ({span + len(A)} rows, "
-                      f"n={n}, bf16->fp64 weight upcast included), scaled x{shape.n_layers / layers:g}; "
+                      f"n={n}, bf16->fp64 weight upcast included), scaled x{shape.n_layers / layers * n_docs:g}"
+                      f"{' (layers x documents)' if n_docs > 1 else ''}; "
                       f"{dt:.1f} s measured"}
 
 
