@@ -167,6 +167,31 @@ typedef enum { KVR_EDIT_LOCAL = 0, KVR_RANDOM = 1 } kvr_policy;
 kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_start, int32_t edit_end,
                       int32_t K, uint64_t seed, int32_t *h_out, int32_t *n_out);
 
+/* EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"): the
+ * structural variant that recomputes from the end of the edit to the next
+ * document boundary, with no selector forward.  Returns the positions
+ * [edit_end, min(boundary, n - 1)) of the pool D = [edit_end, n - 1) in
+ * ascending order; `boundary` is the position where the next document
+ * begins (boundary == edit_end selects nothing).  h_out must hold `capacity`
+ * entries.  Errors: KVR_E_ARG (NULL outputs or capacity < 0), KVR_E_RANGE
+ * (n < 1, not 0 <= edit_start <= edit_end <= n, boundary < edit_end, or more
+ * than `capacity` positions; nothing is written then). */
+kvr_status kvr_select_to_boundary(int32_t n, int32_t edit_start, int32_t edit_end, int32_t boundary,
+                                  int32_t capacity, int32_t *h_out, int32_t *n_out);
+
+/* Transplant (Section 3, "Transplant is not recomputation"): copy the key and
+ * value rows of the given positions, every layer and kv head, from d_src (for
+ * the diagnostic: the oracle cache K(C')) into d_dst (the stale cache).  A
+ * localization diagnostic that needs the oracle cache, not a repair method.
+ * Both caches use the layout of kvr_prefill with their own n_cap; positions
+ * (host array, copied during the call) must lie in [0, min(src_n_cap,
+ * dst_n_cap)) and be strictly ascending.  Enqueued on `stream` as device
+ * copies, one per run of consecutive positions.  Errors: KVR_E_ARG (NULL
+ * context or caches, unsorted positions, misaligned caches), KVR_E_RANGE
+ * (a position out of range), KVR_E_HIP. */
+kvr_status kvr_transplant(kvr_ctx *ctx, const void *d_src, int32_t src_n_cap, void *d_dst, int32_t dst_n_cap,
+                          const int32_t *h_positions, int32_t n_positions, void *stream);
+
 /* Per-step GPU time accounting, a tracing aid for benchmarks.  While enabled
  * (it is off after kvr_create), every kernel launch of a prefill or repair
  * pass is made with a pair of HIP events that the dispatch records at the

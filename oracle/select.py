@@ -68,3 +68,13 @@ def select_random(n: int, edit_start: int, edit_end: int, k: int, seed: int) -> 
         j = i + rng.next() % (m - i)
         d[i], d[j] = d[j], d[i]
     return sorted(d[:kk])
+
+
+def select_to_boundary(n: int, edit_start: int, edit_end: int, boundary: int) -> List[int]:
+    """EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"):
+    every pool position from the end of the edit up to the next document
+    boundary, i.e. [s_end, min(boundary, n - 1)) -- the pool D ends at n - 1."""
+    check_span(n, edit_start, edit_end, 0)
+    if boundary < edit_end:
+        raise ValueError("boundary before the end of the edit")
+    return list(range(edit_end, min(boundary, n - 1)))

@@ -23,7 +23,8 @@ STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPO
                 5: "KVR_E_HIP"}
 
 EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
-            "kvr_select", "kvr_profile_enable", "kvr_profile_read", "kvr_last_error")
+            "kvr_select", "kvr_select_to_boundary", "kvr_transplant", "kvr_profile_enable", "kvr_profile_read",
+            "kvr_last_error")
 
 
 class KvrError(RuntimeError):
@@ -83,6 +84,12 @@ def load() -> ctypes.CDLL:
     lib.kvr_repair.restype = c_int
     lib.kvr_select.argtypes = [c_int, c_int32, c_int32, c_int32, c_int32, c_uint64, POINTER(c_int32), POINTER(c_int32)]
     lib.kvr_select.restype = c_int
+    lib.kvr_select_to_boundary.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, POINTER(c_int32),
+                                           POINTER(c_int32)]
+    lib.kvr_select_to_boundary.restype = c_int
+    lib.kvr_transplant.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_int32, POINTER(c_int32), c_int32,
+                                   c_void_p]
+    lib.kvr_transplant.restype = c_int
     lib.kvr_profile_enable.argtypes = [c_void_p, c_int32]
     lib.kvr_profile_enable.restype = c_int
     lib.kvr_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_char_p), POINTER(c_double), POINTER(c_int64),
@@ -162,3 +169,17 @@ def kvr_select(policy: int, n: int, edit_start: int, edit_end: int, K: int, seed
     cnt = c_int32(0)
     _check(load().kvr_select(policy, n, edit_start, edit_end, K, seed & ((1 << 64) - 1), out, ctypes.byref(cnt)))
     return list(out[:cnt.value])
+
+
+def kvr_select_to_boundary(n: int, edit_start: int, edit_end: int, boundary: int, capacity: Optional[int] = None) -> list:
+    cap = max(0, n) if capacity is None else capacity
+    out = (c_int32 * max(1, cap))()
+    cnt = c_int32(0)
+    _check(load().kvr_select_to_boundary(n, edit_start, edit_end, boundary, cap, out, ctypes.byref(cnt)))
+    return list(out[:cnt.value])
+
+
+def kvr_transplant(ctx: int, d_src: int, src_n_cap: int, d_dst: int, dst_n_cap: int, positions: Sequence[int],
+                   stream: Optional[int] = None) -> None:
+    arr = (c_int32 * max(1, len(positions)))(*positions)
+    _check(load().kvr_transplant(ctx, d_src, src_n_cap, d_dst, dst_n_cap, arr, len(positions), stream), ctx)

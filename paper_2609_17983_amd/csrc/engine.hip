@@ -604,6 +604,37 @@ kvr_status kvr_prefill(kvr_ctx *c, const int32_t *d_tokens, int32_t n, int32_t n
     return KVR_OK;
 }
 
+kvr_status kvr_transplant(kvr_ctx *c, const void *d_src, int32_t src_n_cap, void *d_dst, int32_t dst_n_cap,
+                          const int32_t *h_positions, int32_t n_positions, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_transplant: NULL context");
+    if (n_positions < 0 || (n_positions > 0 && !h_positions)) return fail(c, KVR_E_ARG, "kvr_transplant: bad position list");
+    if (n_positions == 0) return KVR_OK;
+    if (!d_src || !d_dst) return fail(c, KVR_E_ARG, "kvr_transplant: NULL cache");
+    if (!aligned16(d_src) || !aligned16(d_dst)) return fail(c, KVR_E_ARG, "kvr_transplant: caches must be 16-byte aligned");
+    const int32_t lim = std::min(src_n_cap, dst_n_cap);
+    for (int i = 0; i < n_positions; ++i) {
+        if (h_positions[i] < 0 || h_positions[i] >= lim) return fail(c, KVR_E_RANGE, "kvr_transplant: position out of range");
+        if (i > 0 && h_positions[i] <= h_positions[i - 1])
+            return fail(c, KVR_E_ARG, "kvr_transplant: positions must be strictly ascending");
+    }
+    DeviceGuard g(c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t row = (size_t)c->d.head_dim * elem_size(c->d);
+    const size_t planes = (size_t)c->d.n_layers * 2 * c->d.n_kv_heads;
+    for (int i = 0; i < n_positions;) {
+        int j = i + 1;
+        while (j < n_positions && h_positions[j] == h_positions[j - 1] + 1) ++j;
+        const size_t p0 = (size_t)h_positions[i];
+        // one 2-D copy: `planes` rows of (j - i) cache rows each
+        hipError_t e = hipMemcpy2DAsync((char *)d_dst + p0 * row, (size_t)dst_n_cap * row,
+                                        (const char *)d_src + p0 * row, (size_t)src_n_cap * row, (size_t)(j - i) * row,
+                                        planes, hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) return hip_fail(c, e, "kvr_transplant: hipMemcpy2DAsync");
+        i = j;
+    }
+    return KVR_OK;
+}
+
 kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {
     if (!c) return fail(nullptr, KVR_E_ARG, "kvr_profile_enable: NULL context");
     c->profiling = enable != 0;

@@ -64,3 +64,25 @@ extern "C" kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_star
     std::copy(pool.begin(), pool.begin() + k, h_out);
     return KVR_OK;
 }
+
+extern "C" kvr_status kvr_select_to_boundary(int32_t n, int32_t edit_start, int32_t edit_end, int32_t boundary,
+                                             int32_t capacity, int32_t *h_out, int32_t *n_out) {
+    if (!n_out || capacity < 0 || (capacity > 0 && !h_out)) {
+        kvr::set_global_error("kvr_select_to_boundary: NULL output or negative capacity");
+        return KVR_E_ARG;
+    }
+    if (n < 1 || edit_start < 0 || edit_start > edit_end || edit_end > n || boundary < edit_end) {
+        kvr::set_global_error("kvr_select_to_boundary: need n >= 1, 0 <= edit_start <= edit_end <= n, "
+                              "boundary >= edit_end");
+        return KVR_E_RANGE;
+    }
+    const int64_t end = std::min<int64_t>(boundary, (int64_t)n - 1);
+    const int64_t k = std::max<int64_t>(0, end - edit_end);
+    if (k > capacity) {
+        kvr::set_global_error("kvr_select_to_boundary: more positions than the output capacity");
+        return KVR_E_RANGE;
+    }
+    for (int64_t i = 0; i < k; ++i) h_out[i] = (int32_t)(edit_end + i);
+    *n_out = (int32_t)k;
+    return KVR_OK;
+}

@@ -135,3 +135,26 @@ def test_null_context_calls():
     assert lib.kvr_repair(None, None, 0, None) == kvr.KVR_E_ARG
     assert lib.kvr_workspace_bytes(None) == 0
     lib.kvr_destroy(None)
+
+
+def test_select_to_boundary_matches_oracle():
+    rnd = random.Random(2)
+    for _ in range(300):
+        n = rnd.randint(1, 9000)
+        s0 = rnd.randint(0, n)
+        s1 = rnd.randint(s0, min(n, s0 + 64))
+        b = s1 + rnd.randint(0, 80)
+        assert kvr.kvr_select_to_boundary(n, s0, s1, b) == osel.select_to_boundary(n, s0, s1, b)
+
+
+def test_select_to_boundary_errors():
+    with pytest.raises(kvr.KvrError) as e:
+        kvr.kvr_select_to_boundary(100, 10, 14, 13)
+    assert e.value.status == kvr.KVR_E_RANGE
+    with pytest.raises(kvr.KvrError) as e:
+        kvr.kvr_select_to_boundary(100, 10, 14, 40, capacity=8)  # 26 positions
+    assert e.value.status == kvr.KVR_E_RANGE
+    assert kvr.kvr_select_to_boundary(100, 10, 14, 40, capacity=26) == list(range(14, 40))
+    lib = kvr.load()
+    assert lib.kvr_select_to_boundary(100, 10, 14, 40, 4, None, None) == kvr.KVR_E_ARG
+    assert lib.kvr_transplant(None, None, 0, None, 0, None, 0, None) == kvr.KVR_E_ARG

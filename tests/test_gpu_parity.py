@@ -137,6 +137,55 @@ def test_tiny_upstream_and_suffix(tiny):
     assert relmax(hidden.cpu().numpy(), oy[128:]) <= TOL[kvr.KVR_F32]
 
 
+def test_transplant_matches_oracle(tiny):
+    """Transplant (Section 3, "Transplant is not recomputation"): the rows of
+    the given positions come from K(C') bit for bit, every layer and kv head;
+    all other rows stay the stale cache's.  The source cache has a larger
+    capacity than the destination."""
+    shape, eng, ow, toks, new, stale_np, _ = tiny
+    oracle_np, _ = od.prefill(shape, ow, new.numpy())
+    n = stale_np.shape[3]
+    pos = [0, 1, 2, 127, 128, 129, 130, 200, 301, 302, n - 1]
+    stream = torch.cuda.current_stream().cuda_stream
+    dst = torch.from_numpy(stale_np).float().cuda()
+    src = torch.zeros((shape.n_layers, 2, shape.n_kv_heads, n + 40, shape.head_dim), dtype=torch.float32,
+                      device="cuda")
+    src[:, :, :, :n] = torch.from_numpy(oracle_np).float().cuda()
+    kvr.kvr_transplant(eng.ctx, src.data_ptr(), n + 40, dst.data_ptr(), n, pos, stream)
+    ref = stale_np.astype(np.float32)
+    od.transplant(ref, oracle_np.astype(np.float32), pos)
+    torch.cuda.synchronize()
+    assert np.array_equal(dst.cpu().numpy(), ref)
+    # every position: the destination becomes K(C')
+    full = torch.from_numpy(stale_np).float().cuda()
+    kvr.kvr_transplant(eng.ctx, src.data_ptr(), n + 40, full.data_ptr(), n, list(range(n)), stream)
+    torch.cuda.synchronize()
+    assert np.array_equal(full.cpu().numpy(), oracle_np.astype(np.float32))
+    # rejected calls leave the destination untouched
+    before = dst.clone()
+    for bad, status in (([n], kvr.KVR_E_RANGE), ([5, 4], kvr.KVR_E_ARG), ([-1], kvr.KVR_E_RANGE)):
+        with pytest.raises(kvr.KvrError) as e:
+            kvr.kvr_transplant(eng.ctx, src.data_ptr(), n + 40, dst.data_ptr(), n, bad, stream)
+        assert e.value.status == status
+    kvr.kvr_transplant(eng.ctx, src.data_ptr(), n + 40, dst.data_ptr(), n, [], stream)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, before)
+
+
+def test_transplant_bf16(mid):
+    shape, eng, ow, toks, new, stale_np = mid
+    n = stale_np.shape[3]
+    rng = np.random.default_rng(3)
+    pos = sorted(rng.choice(n, size=57, replace=False).tolist())
+    src = torch.randn((shape.n_layers, 2, shape.n_kv_heads, n, shape.head_dim), device="cuda").to(torch.bfloat16)
+    dst = torch.from_numpy(stale_np).to(torch.bfloat16).cuda()
+    ref = dst.clone()
+    ref[:, :, :, pos] = src[:, :, :, pos]
+    kvr.kvr_transplant(eng.ctx, src.data_ptr(), n, dst.data_ptr(), n, pos, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, ref)
+
+
 def test_tiny_empty_edit_is_noop(tiny):
     shape, eng, ow, toks, new, stale_np, _ = tiny
     cache = torch.from_numpy(stale_np).float().cuda()

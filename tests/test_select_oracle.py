@@ -81,3 +81,17 @@ def test_random_first_draw_by_hand():
     # D = [2, 3, 4, 5, 6] (n = 8, span [1, 2)); K = 1 picks D[next() mod 5]
     first = osel.SplitMix64(7).next()
     assert osel.select_random(8, 1, 2, 1, 7) == [2 + first % 5]
+
+
+def test_to_boundary_is_edit_local_up_to_the_boundary():
+    """EditLocal@boundary (Section 5.2) recomputes from the edit end to the next
+    document boundary: it equals EditLocal with K = boundary - s_end while the
+    boundary lies inside the pool, and the pool end n-1 clips it otherwise."""
+    for n, s0, s1 in ((5000, 1500, 1516), (64, 10, 14), (20, 0, 0)):
+        for k in range(0, 40):
+            b = s1 + k
+            assert osel.select_to_boundary(n, s0, s1, b) == osel.select_edit_local(n, s0, s1, k)
+    assert osel.select_to_boundary(64, 10, 14, 14) == []
+    assert osel.select_to_boundary(64, 10, 14, 10 ** 6) == list(range(14, 63))
+    with pytest.raises(ValueError):
+        osel.select_to_boundary(64, 10, 14, 13)
