@@ -90,18 +90,23 @@ typedef struct {
 } kvr_layer_weights;
 
 /* embed [vocab][d_model] and final_norm [d_model] on the device; `layers` is a
- * HOST array of n_layers entries (copied by kvr_create). */
+ * HOST array of n_layers entries (copied by kvr_create); lm_head
+ * [vocab][d_model] is the output projection used only by kvr_score and
+ * kvr_generate (NULL: tied to embed). */
 typedef struct {
     const void *embed, *final_norm;
     const kvr_layer_weights *layers;
+    const void *lm_head;
 } kvr_weights;
 
 typedef struct kvr_ctx kvr_ctx;
 
 /* Create a context on the current HIP device.  The weight pointers are
  * borrowed (not copied) and must stay valid until kvr_destroy.  The context
- * allocates its workspace (sized from max_rows, max_ctx and the model dims;
- * kvr_workspace_bytes reports it) and a pinned host staging buffer.
+ * allocates its workspace (sized from max_rows, max_ctx and the model dims),
+ * a pinned host staging buffer and, in bf16, a copy of every projection
+ * matrix and of the LM head repacked in MFMA operand order (about the size of
+ * the model's matrices); kvr_workspace_bytes reports the device total.
  * Errors: KVR_E_ARG (NULL/invalid dims or misaligned/missing weights),
  * KVR_E_UNSUPPORTED, KVR_E_NOMEM, KVR_E_HIP.  On error *out is NULL and the
  * message is available through kvr_last_error(NULL). */
@@ -167,6 +172,36 @@ typedef enum { KVR_EDIT_LOCAL = 0, KVR_RANDOM = 1 } kvr_policy;
 kvr_status kvr_select(kvr_policy policy, int32_t n, int32_t edit_start, int32_t edit_end,
                       int32_t K, uint64_t seed, int32_t *h_out, int32_t *n_out);
 
+/* Fresh-query forward and teacher-forced scoring over a (repaired) cache
+ * (Section 3, "What counts as repaired": the margin m_x is the difference of
+ * the length-averaged teacher-forced log-probabilities of two answers; Eq. 2
+ * and Eq. 3 are computed from it and from kvr_generate).  The m tokens
+ * d_tokens[n .. n+m) are appended after the n cached positions: they run
+ * through the decoder attending over cache rows [0, n) and causally over each
+ * other, their keys/values are written into cache slots [n, n+m) (scratch:
+ * rows [0, n) are not touched), and the LM head and a log-softmax over the
+ * vocabulary follow.  Outputs (device): for j < m-1,
+ *   d_logprob[j] = log p(d_tokens[n+j+1] | d_tokens[0 .. n+j]),
+ * and for j < m, d_argmax[j] = the most probable token after position n+j
+ * (lowest id among equal maxima); d_argmax may be NULL, d_logprob may be NULL
+ * only when m == 1.  Errors: KVR_E_ARG (NULL context, cache or tokens,
+ * misaligned cache), KVR_E_RANGE (not 0 <= n, 1 <= m, n + m <= n_cap <=
+ * max_ctx, or m above the context's pass size), KVR_E_NOMEM (the first call
+ * allocates the scoring buffers), KVR_E_HIP. */
+kvr_status kvr_score(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens, int32_t m,
+                     float *d_logprob, int32_t *d_argmax, void *stream);
+
+/* Greedy continuation (the generation y_b of Eq. 3): appends the q query
+ * tokens d_tokens[n .. n+q) after the n cached positions as kvr_score does,
+ * then generates max_new tokens one at a time, each the most probable token
+ * after the previous one (lowest id among equal maxima), and writes them to
+ * d_tokens[n+q .. n+q+max_new).  The whole loop is enqueued on `stream`: each
+ * generated id is written on the device and read by the next step's forward.
+ * Cache slots [n, n+q+max_new-1) are scratch.  Errors as kvr_score, with
+ * KVR_E_RANGE unless 1 <= q, 1 <= max_new and n + q + max_new - 1 <= n_cap. */
+kvr_status kvr_generate(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, int32_t *d_tokens, int32_t q,
+                        int32_t max_new, void *stream);
+
 /* EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"): the
  * structural variant that recomputes from the end of the edit to the next
  * document boundary, with no selector forward.  Returns the positions
@@ -198,7 +233,8 @@ kvr_status kvr_transplant(kvr_ctx *ctx, const void *d_src, int32_t src_n_cap, vo
  * start and at the end of the kernel's execution (hipExtLaunchKernel), tagged
  * with the step of the layer loop it belongs to ("embed", "rmsnorm",
  * "qkv_proj", "rope_scatter", "attention", "attention_combine", "o_proj",
- * "gate_up_swiglu", "down_proj", "final_norm").  The time of a launch is its
+ * "gate_up_swiglu", "down_proj", "final_norm", and for the scoring calls
+ * "lm_head", "logsoftmax").  The time of a launch is its
  * execution time; the dispatch gaps between kernels are not counted, so the
  * step times sum to less than the pass.  Errors: KVR_E_ARG (NULL context). */
 kvr_status kvr_profile_enable(kvr_ctx *ctx, int32_t enable);

@@ -23,8 +23,8 @@ STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPO
                 5: "KVR_E_HIP"}
 
 EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
-            "kvr_select", "kvr_select_to_boundary", "kvr_transplant", "kvr_profile_enable", "kvr_profile_read",
-            "kvr_last_error")
+            "kvr_select", "kvr_select_to_boundary", "kvr_transplant", "kvr_score", "kvr_generate",
+            "kvr_profile_enable", "kvr_profile_read", "kvr_last_error")
 
 
 class KvrError(RuntimeError):
@@ -46,7 +46,8 @@ class kvr_layer_weights(ctypes.Structure):
 
 
 class kvr_weights(ctypes.Structure):
-    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p), ("layers", POINTER(kvr_layer_weights))]
+    _fields_ = [("embed", c_void_p), ("final_norm", c_void_p), ("layers", POINTER(kvr_layer_weights)),
+                ("lm_head", c_void_p)]
 
 
 class kvr_doc(ctypes.Structure):
@@ -90,6 +91,10 @@ def load() -> ctypes.CDLL:
     lib.kvr_transplant.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_int32, POINTER(c_int32), c_int32,
                                    c_void_p]
     lib.kvr_transplant.restype = c_int
+    lib.kvr_score.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
+    lib.kvr_score.restype = c_int
+    lib.kvr_generate.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_int32, c_int32, c_void_p]
+    lib.kvr_generate.restype = c_int
     lib.kvr_profile_enable.argtypes = [c_void_p, c_int32]
     lib.kvr_profile_enable.restype = c_int
     lib.kvr_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_char_p), POINTER(c_double), POINTER(c_int64),
@@ -183,3 +188,13 @@ def kvr_transplant(ctx: int, d_src: int, src_n_cap: int, d_dst: int, dst_n_cap: 
                    stream: Optional[int] = None) -> None:
     arr = (c_int32 * max(1, len(positions)))(*positions)
     _check(load().kvr_transplant(ctx, d_src, src_n_cap, d_dst, dst_n_cap, arr, len(positions), stream), ctx)
+
+
+def kvr_score(ctx: int, d_cache: int, n: int, n_cap: int, d_tokens: int, m: int, d_logprob: Optional[int],
+              d_argmax: Optional[int] = None, stream: Optional[int] = None) -> None:
+    _check(load().kvr_score(ctx, d_cache, n, n_cap, d_tokens, m, d_logprob, d_argmax, stream), ctx)
+
+
+def kvr_generate(ctx: int, d_cache: int, n: int, n_cap: int, d_tokens: int, q: int, max_new: int,
+                 stream: Optional[int] = None) -> None:
+    _check(load().kvr_generate(ctx, d_cache, n, n_cap, d_tokens, q, max_new, stream), ctx)

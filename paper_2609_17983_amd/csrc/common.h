@@ -188,6 +188,15 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
 hipError_t launch_pack_weight(const void *w0, const void *w1, const void *w2, int e0, int e1, bool interleave,
                               int V, int K, void *dst, hipStream_t s);
 
+// Scoring rows: hidden rows Y [R][d] fp32 -> LM-head operand (compensated
+// bf16 pair, operand order or row-major, or fp32 row-major).
+hipError_t launch_to_operand(bool bf16, bool perm, const float *Y, int R, int d, void *X, void *X_lo, hipStream_t s);
+// Log-softmax of R rows of V logits (sum of nsplit fp32 tiles part[s][R][V]):
+// lp[r] = log p(target[r]) for r < n_targets, argmax[r] (lowest index among
+// maxima; argmax may be null), next[0] = argmax of row R-1 when next is given.
+hipError_t launch_logsoftmax(const float *part, int nsplit, int R, int V, const int32_t *target, int n_targets,
+                             float *lp, int32_t *argmax, int32_t *next, hipStream_t s);
+
 // Attention item geometry shared by the planner and the kernels.
 constexpr int ATT_KT = 64;     // keys per LDS tile
 constexpr int ATT_HD = 128;    // head_dim of the MFMA attention kernel

@@ -47,6 +47,15 @@ struct kvr_ctx {
     char *wpk = nullptr;
     size_t wpk_bytes = 0;
 
+    // scoring: LM head (borrowed; the embedding when tied), its packed copy,
+    // and buffers made on the first kvr_score / kvr_generate call
+    const void *lm_head = nullptr;
+    void *lm_pk = nullptr;
+    size_t lm_pk_bytes = 0;
+    float *score_y = nullptr;     // hidden rows of the scored block [max rows][d]
+    float *score_part = nullptr;  // logit tiles [split][64][vocab]
+    size_t score_bytes = 0;
+
     int rows_cap = 0;  // rows per pass
     int max_docs = 0;
     int items_cap = 0, comb_cap = 0;
@@ -85,9 +94,14 @@ constexpr size_t ATTN_PART_BYTES = 64ull << 20;
 constexpr int PART_ROW = ATT_HD + 4;
 constexpr int SPLIT_MAX = 32;
 
-enum Step { ST_EMBED, ST_NORM, ST_QKV, ST_ROPE, ST_ATTN, ST_COMBINE, ST_OPROJ, ST_GATEUP, ST_DOWN, ST_FINAL, ST_COUNT };
+enum Step {
+    ST_EMBED, ST_NORM, ST_QKV, ST_ROPE, ST_ATTN, ST_COMBINE, ST_OPROJ, ST_GATEUP, ST_DOWN, ST_FINAL, ST_LMHEAD,
+    ST_LOGSOFTMAX, ST_COUNT
+};
 const char *const STEP_NAMES[ST_COUNT] = {"embed", "rmsnorm", "qkv_proj", "rope_scatter", "attention",
-                                          "attention_combine", "o_proj", "gate_up_swiglu", "down_proj", "final_norm"};
+                                          "attention_combine", "o_proj", "gate_up_swiglu", "down_proj", "final_norm",
+                                          "lm_head", "logsoftmax"};
+constexpr int SCORE_ROWS = 64;  // rows per LM-head launch (the skinny kernel's bound)
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -392,6 +406,74 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
     return KVR_OK;
 }
 
+// Forward over the m rows at positions [n, n+m) of one document (their keys
+// and values land in cache slots [n, n+m)), then the LM head and the
+// log-softmax in blocks of SCORE_ROWS rows: lp[j] = log p(tokens[n+j+1]) for
+// j < m-1, argmax[j] for j < m, and *next = argmax of row m-1.
+kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t *tokens, int m, float *lp,
+                       int32_t *argmax, int32_t *next, hipStream_t s) {
+    const kvr_dims &d = c->d;
+    const int D = d.d_model, V = d.vocab;
+    Tables t;
+    t.docs.push_back(DocInfo{cache, tokens, c->score_y, n + m, n_cap, 0, m});
+    t.rows.reserve(m);
+    for (int j = 0; j < m; ++j) t.rows.push_back(RowInfo{n + j, 0, j, 0});
+    kvr_status st = run_pass(c, t, s);
+    if (st != KVR_OK) return st;
+    const SkinnyPlan plan = plan_skinny(V / 16, D, false, "KVR_NT_LM", "KVR_SPLIT_LM");
+#define KVR_SCHECK(expr, what, step)                                                \
+    do {                                                                           \
+        hipError_t err_ = arm(c);                                                  \
+        const LaunchTimer armed_ = launch_timer();                                 \
+        if (err_ == hipSuccess) err_ = (expr);                                     \
+        disarm(c, step, armed_.start, armed_.stop);                                \
+        if (err_ != hipSuccess) return hip_fail(c, err_, what);                    \
+    } while (0)
+    for (int c0 = 0; c0 < m; c0 += SCORE_ROWS) {
+        const int R = std::min(SCORE_ROWS, m - c0);
+        const float *Y = c->score_y + (size_t)c0 * D;
+        int nsplit = 1;
+        if (c->lm_pk) {
+            KVR_SCHECK(launch_to_operand(true, true, Y, R, D, c->Xn, c->Xn_lo, s), "lm_head operand", ST_LMHEAD);
+            KVR_SCHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, V, c->lm_pk, c->score_part, nullptr, plan, s),
+                       "lm_head", ST_LMHEAD);
+            nsplit = plan.split;
+        } else if (c->bf16) {
+            KVR_SCHECK(launch_to_operand(true, false, Y, R, D, c->Xn, c->Xn_lo, s), "lm_head operand", ST_LMHEAD);
+            KVR_SCHECK(launch_linear_simple(true, EPI_STORE, make_args(c->Xn, c->Xn_lo, D, R, D, V, c->lm_head,
+                                                                       c->lm_head, c->lm_head, V, V, nullptr,
+                                                                       c->score_part, nullptr, V), s),
+                       "lm_head", ST_LMHEAD);
+        } else {
+            KVR_SCHECK(launch_linear_simple(false, EPI_STORE, make_args(Y, nullptr, D, R, D, V, c->lm_head, c->lm_head,
+                                                                        c->lm_head, V, V, nullptr, c->score_part,
+                                                                        nullptr, V), s),
+                       "lm_head", ST_LMHEAD);
+        }
+        const int nt = lp ? std::max(0, std::min(R, m - 1 - c0)) : 0;  // rows with a target to score
+        KVR_SCHECK(launch_logsoftmax(c->score_part, nsplit, R, V, tokens + n + c0 + 1, nt, lp ? lp + c0 : nullptr,
+                                     argmax ? argmax + c0 : nullptr, (c0 + R == m) ? next : nullptr, s),
+                   "logsoftmax", ST_LOGSOFTMAX);
+    }
+#undef KVR_SCHECK
+    return KVR_OK;
+}
+
+kvr_status score_buffers(kvr_ctx *c) {
+    if (c->score_y) return KVR_OK;
+    const kvr_dims &d = c->d;
+    const SkinnyPlan plan = plan_skinny(d.vocab / 16, d.d_model, false, "KVR_NT_LM", "KVR_SPLIT_LM");
+    const size_t y_bytes = align_up((size_t)c->rows_cap * d.d_model * 4, 256);
+    const size_t p_bytes = (size_t)std::max(plan.split, 1) * SCORE_ROWS * d.vocab * 4;
+    char *buf = nullptr;
+    hipError_t e = hipMalloc((void **)&buf, y_bytes + p_bytes);
+    if (e != hipSuccess) return fail(c, KVR_E_NOMEM, "scoring buffer allocation failed");
+    c->score_y = (float *)buf;
+    c->score_part = (float *)(buf + y_bytes);
+    c->score_bytes = y_bytes + p_bytes;
+    return KVR_OK;
+}
+
 kvr_status check_dims(const kvr_dims *d) {
     if (!d) return KVR_E_ARG;
     if (d->n_layers < 1 || d->d_model < 1 || d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 2 ||
@@ -413,7 +495,7 @@ size_t kvr_cache_bytes(const kvr_dims *d, int32_t n_cap) {
     return (size_t)d->n_layers * 2 * d->n_kv_heads * (size_t)n_cap * d->head_dim * elem_size(*d);
 }
 
-size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes + c->wpk_bytes : 0; }
+size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes + c->wpk_bytes + c->lm_pk_bytes + c->score_bytes : 0; }
 
 const char *kvr_last_error(const kvr_ctx *c) { return c ? c->err.c_str() : g_error.c_str(); }
 
@@ -427,7 +509,7 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     if (!wts || !wts->embed || !wts->final_norm || !wts->layers)
         return fail(nullptr, KVR_E_ARG, "kvr_create: NULL weights");
     const kvr_dims &d = *dims;
-    if (!aligned16(wts->embed) || !aligned16(wts->final_norm))
+    if (!aligned16(wts->embed) || !aligned16(wts->final_norm) || (wts->lm_head && !aligned16(wts->lm_head)))
         return fail(nullptr, KVR_E_ARG, "kvr_create: weights must be 16-byte aligned");
     for (int l = 0; l < d.n_layers; ++l) {
         const kvr_layer_weights &w = wts->layers[l];
@@ -450,6 +532,7 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     c->layers.assign(wts->layers, wts->layers + d.n_layers);
     c->embed = wts->embed;
     c->final_norm = wts->final_norm;
+    c->lm_head = wts->lm_head ? wts->lm_head : wts->embed;
     hipError_t e = hipGetDevice(&c->device);
     if (e != hipSuccess) { delete c; return hip_fail(nullptr, e, "hipGetDevice"); }
 
@@ -553,8 +636,15 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
             if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, dst, 0);
             dst += (size_t)D * F;
         }
+        if (e == hipSuccess && d.vocab % 16 == 0) {
+            c->lm_pk_bytes = (size_t)d.vocab * D * 2;
+            e = hipMalloc(&c->lm_pk, c->lm_pk_bytes);
+            if (e == hipSuccess) e = launch_pack_weight(c->lm_head, c->lm_head, c->lm_head, d.vocab, d.vocab, false,
+                                                        d.vocab, D, c->lm_pk, 0);
+        }
         if (e == hipSuccess) e = hipStreamSynchronize(0);
         if (e != hipSuccess) {
+            if (c->lm_pk) (void)hipFree(c->lm_pk);
             (void)hipFree(c->wpk);
             (void)hipEventDestroy(c->stage_ev); (void)hipHostFree(c->h_stage); (void)hipFree(c->ws); delete c;
             return hip_fail(nullptr, e, "kvr_create: weight packing");
@@ -578,6 +668,8 @@ void kvr_destroy(kvr_ctx *c) {
         if (c->h_stage) (void)hipHostFree(c->h_stage);
         if (c->ws) (void)hipFree(c->ws);
         if (c->wpk) (void)hipFree(c->wpk);
+        if (c->lm_pk) (void)hipFree(c->lm_pk);
+        if (c->score_y) (void)hipFree(c->score_y);
     }
     delete c;
 }
@@ -633,6 +725,41 @@ kvr_status kvr_transplant(kvr_ctx *c, const void *d_src, int32_t src_n_cap, void
         i = j;
     }
     return KVR_OK;
+}
+
+kvr_status kvr_score(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens, int32_t m,
+                     float *d_logprob, int32_t *d_argmax, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_score: NULL context");
+    if (!d_cache || !d_tokens) return fail(c, KVR_E_ARG, "kvr_score: NULL cache or tokens");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_score: cache must be 16-byte aligned");
+    if (m > 1 && !d_logprob) return fail(c, KVR_E_ARG, "kvr_score: NULL log-probability output");
+    if (n < 0 || m < 1 || (long long)n + m > n_cap || n_cap > c->d.max_ctx)
+        return fail(c, KVR_E_RANGE, "kvr_score: need n >= 0, m >= 1, n + m <= n_cap <= max_ctx");
+    if (m > c->rows_cap) return fail(c, KVR_E_RANGE, "kvr_score: more appended tokens than one pass holds");
+    DeviceGuard g(c->device);
+    kvr_status st = score_buffers(c);
+    if (st != KVR_OK) return st;
+    return score_block(c, d_cache, n, n_cap, d_tokens, m, d_logprob, d_argmax, nullptr, (hipStream_t)stream);
+}
+
+kvr_status kvr_generate(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, int32_t *d_tokens, int32_t q,
+                        int32_t max_new, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_generate: NULL context");
+    if (!d_cache || !d_tokens) return fail(c, KVR_E_ARG, "kvr_generate: NULL cache or tokens");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_generate: cache must be 16-byte aligned");
+    if (n < 0 || q < 1 || max_new < 1 || (long long)n + q + max_new - 1 > n_cap || n_cap > c->d.max_ctx)
+        return fail(c, KVR_E_RANGE, "kvr_generate: need n >= 0, q >= 1, max_new >= 1, n + q + max_new - 1 <= n_cap <= max_ctx");
+    if (q > c->rows_cap) return fail(c, KVR_E_RANGE, "kvr_generate: query longer than one pass holds");
+    DeviceGuard g(c->device);
+    kvr_status st = score_buffers(c);
+    if (st != KVR_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    // the query block, then one row per generated token; every next id is
+    // written on the device and read back by the following pass
+    st = score_block(c, d_cache, n, n_cap, d_tokens, q, nullptr, nullptr, d_tokens + n + q, s);
+    for (int i = 1; i < max_new && st == KVR_OK; ++i)
+        st = score_block(c, d_cache, n + q + i - 1, n_cap, d_tokens, 1, nullptr, nullptr, d_tokens + n + q + i, s);
+    return st;
 }
 
 kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {

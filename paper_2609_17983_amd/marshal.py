@@ -18,7 +18,8 @@ def dims_for(shape, dtype: int, max_ctx: int, max_rows: int) -> _lib.kvr_dims:
 
 
 def weights_struct(weights: Dict[str, object]) -> _lib.kvr_weights:
-    """kvr_weights from {'embed', 'final_norm', 'layers': [dict of tensors]} on the device.
+    """kvr_weights from {'embed', 'final_norm', 'layers': [dict of tensors],
+    optionally 'lm_head'} on the device.
 
     The returned struct keeps its layer array alive; the tensors must outlive
     the context created from it.
@@ -29,7 +30,9 @@ def weights_struct(weights: Dict[str, object]) -> _lib.kvr_weights:
         for f in _LAYER_FIELDS:
             t = lw.get(f)
             setattr(arr[i], f, None if t is None else t.data_ptr())
+    lm = weights.get("lm_head")
     ws = _lib.kvr_weights(weights["embed"].data_ptr(), weights["final_norm"].data_ptr(),
-                          ctypes.cast(arr, ctypes.POINTER(_lib.kvr_layer_weights)))
+                          ctypes.cast(arr, ctypes.POINTER(_lib.kvr_layer_weights)),
+                          None if lm is None else lm.data_ptr())
     ws._layers = arr
     return ws

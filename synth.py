@@ -149,6 +149,12 @@ def make_layer_weights(shape: ModelShape, layer: int, dtype: torch.dtype, device
     return w
 
 
+def make_lm_head(shape: ModelShape, dtype: torch.dtype = torch.bfloat16, device: str = "cpu",
+                 seed: int = SEED_WEIGHTS, std: float = 0.02) -> torch.Tensor:
+    """Random-init output projection [vocab][d_model] (untied from the embedding)."""
+    return _normal((shape.vocab, shape.d_model), std, 0.0, dtype, device, _mix_seed(seed, 1 << 21, 0))
+
+
 def make_tokens(n: int, vocab: int, seed: int = SEED_TOKENS, device: str = "cpu") -> torch.Tensor:
     """n uniform token ids in [0, vocab), int32."""
     g = _generator("cpu", _mix_seed(seed, n, vocab))

@@ -158,3 +158,14 @@ def test_select_to_boundary_errors():
     lib = kvr.load()
     assert lib.kvr_select_to_boundary(100, 10, 14, 40, 4, None, None) == kvr.KVR_E_ARG
     assert lib.kvr_transplant(None, None, 0, None, 0, None, 0, None) == kvr.KVR_E_ARG
+
+
+def test_metrics_closed_forms():
+    from paper_2609_17983_amd import metrics
+    assert metrics.answer_logprob([-9.0, -1.0, -2.0, -3.0, -7.0], 2, 3) == -2.0
+    assert metrics.margin(-1.0, -3.0) == 2.0
+    assert metrics.margin_recovery(3.0, 1.0, 5.0) == 0.5
+    assert metrics.margin_recovery(-1.0, 1.0, 5.0) == -0.5
+    assert metrics.margin_recovery(2.0, 1.0, 1.0) is None
+    assert metrics.flipped([5, 6, 7, 8], [6, 7], [9]) and not metrics.flipped([5, 6, 7, 8], [6, 7], [8])
+    assert metrics.flip_rate([([1, 2], [2], [3]), ([1, 2], [3], [1])]) == 0.5
