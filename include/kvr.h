@@ -202,6 +202,25 @@ kvr_status kvr_score(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, cons
 kvr_status kvr_generate(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, int32_t *d_tokens, int32_t q,
                         int32_t max_new, void *stream);
 
+/* CacheBlend selector (Table 1: top-K by the key/value deviation of one early
+ * layer; Section 3, "Cost accounting": about one prefill layer over the
+ * changed suffix).  Runs the positions [edit_start, n) of C' (d_tokens_new,
+ * n ids) through layers 0 .. layer-1 and the key/value projection of `layer`
+ * into a context-owned scratch copy (the stale cache d_cache is only read;
+ * its rows before edit_start stand in for the fresh ones, which the edit
+ * cannot change), then for every pool position p in D = [edit_end, n - 1)
+ *   dev = ||K_fresh[p] - K_stale[p]||_2 + ||V_fresh[p] - V_stale[p]||_2
+ * (norms over all kv heads and dimensions of `layer`), and writes to d_out
+ * (device, K entries) the min(K, |D|) positions of largest deviation (ties:
+ * lower position) in ascending order; *n_out (host) receives that count.  The
+ * paper's "layer 2" is layer = 1 (counting from one).  d_dev_out (device,
+ * |D| floats, or NULL) receives the deviations of D in position order.
+ * Errors: KVR_E_ARG (NULL argument, negative K, misaligned cache),
+ * KVR_E_RANGE (bad n/n_cap/span or layer), KVR_E_NOMEM, KVR_E_HIP. */
+kvr_status kvr_select_cacheblend(kvr_ctx *ctx, const void *d_cache, int32_t n, int32_t n_cap,
+                                 const int32_t *d_tokens_new, int32_t edit_start, int32_t edit_end, int32_t K,
+                                 int32_t layer, int32_t *d_out, float *d_dev_out, int32_t *n_out, void *stream);
+
 /* EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"): the
  * structural variant that recomputes from the end of the edit to the next
  * document boundary, with no selector forward.  Returns the positions

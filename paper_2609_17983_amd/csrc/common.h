@@ -197,6 +197,14 @@ hipError_t launch_to_operand(bool bf16, bool perm, const float *Y, int R, int d,
 hipError_t launch_logsoftmax(const float *part, int nsplit, int R, int V, const int32_t *target, int n_targets,
                              float *lp, int32_t *argmax, int32_t *next, hipStream_t s);
 
+// CacheBlend selector: dev[p - p0] = ||K_fresh[p] - K_stale[p]|| + ||V_fresh[p] -
+// V_stale[p]|| over layer fl of `fresh` and layer sl of `stale` (cache
+// layouts with their own n_cap), p in [p0, p1).
+hipError_t launch_kv_deviation(bool bf16, const void *fresh, int fresh_ncap, int fl, const void *stale, int stale_ncap,
+                               int sl, int Hkv, int hd, int p0, int p1, float *dev, hipStream_t s);
+// The K largest of dev[0, m) (ties: lower index), as ascending positions p0 + i.
+hipError_t launch_topk(const float *dev, int m, int K, int p0, int32_t *out, hipStream_t s);
+
 // Attention item geometry shared by the planner and the kernels.
 constexpr int ATT_KT = 64;     // keys per LDS tile
 constexpr int ATT_HD = 128;    // head_dim of the MFMA attention kernel

@@ -52,6 +52,8 @@ struct kvr_ctx {
     const void *lm_head = nullptr;
     void *lm_pk = nullptr;
     size_t lm_pk_bytes = 0;
+    char *sel_scratch = nullptr;  // CacheBlend: fresh keys/values of the first layers + deviations
+    size_t sel_bytes = 0;
     float *score_y = nullptr;     // hidden rows of the scored block [max rows][d]
     float *score_part = nullptr;  // logit tiles [split][64][vocab]
     size_t score_bytes = 0;
@@ -288,8 +290,10 @@ void disarm(kvr_ctx *c, int step, hipEvent_t start, hipEvent_t stop) {
     }
 }
 
-// Upload the tables of a pass and enqueue its kernels.
-kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
+// Upload the tables of a pass and enqueue its kernels.  kv_layer >= 0 stops
+// the pass at that layer once its fresh keys/values are in the cache (layers
+// below it run in full; no final norm).
+kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1) {
     const kvr_dims &d = c->d;
     const int R = (int)t.rows.size();
     if (R == 0) return KVR_OK;
@@ -345,7 +349,8 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
 
     KVR_CHECK(launch_embed(bf, rows, docs, R, c->embed, D, d.vocab, c->H, s), "embed", ST_EMBED);
     int resid_split = 0;  // partial tiles in P still to be added to H
-    for (int l = 0; l < d.n_layers; ++l) {
+    const int n_run = kv_layer >= 0 ? kv_layer + 1 : d.n_layers;
+    for (int l = 0; l < n_run; ++l) {
         const kvr_layer_weights &w = c->layers[l];
         const kvr_ctx::PackedLayer pw = c->wpk ? c->pk[l] : kvr_ctx::PackedLayer{nullptr, nullptr, nullptr, nullptr};
         KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
@@ -362,6 +367,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s) {
         }
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
                                       hd, c->rope_cos, c->rope_sin, c->Qb, c->Qb_lo, s), "rope_scatter", ST_ROPE);
+        if (l == kv_layer) return KVR_OK;
         if (attn_mfma) {
             KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, docs, items,
                                             (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
@@ -495,7 +501,9 @@ size_t kvr_cache_bytes(const kvr_dims *d, int32_t n_cap) {
     return (size_t)d->n_layers * 2 * d->n_kv_heads * (size_t)n_cap * d->head_dim * elem_size(*d);
 }
 
-size_t kvr_workspace_bytes(const kvr_ctx *c) { return c ? c->ws_bytes + c->wpk_bytes + c->lm_pk_bytes + c->score_bytes : 0; }
+size_t kvr_workspace_bytes(const kvr_ctx *c) {
+    return c ? c->ws_bytes + c->wpk_bytes + c->lm_pk_bytes + c->score_bytes + c->sel_bytes : 0;
+}
 
 const char *kvr_last_error(const kvr_ctx *c) { return c ? c->err.c_str() : g_error.c_str(); }
 
@@ -670,6 +678,7 @@ void kvr_destroy(kvr_ctx *c) {
         if (c->wpk) (void)hipFree(c->wpk);
         if (c->lm_pk) (void)hipFree(c->lm_pk);
         if (c->score_y) (void)hipFree(c->score_y);
+        if (c->sel_scratch) (void)hipFree(c->sel_scratch);
     }
     delete c;
 }
@@ -760,6 +769,66 @@ kvr_status kvr_generate(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, int
     for (int i = 1; i < max_new && st == KVR_OK; ++i)
         st = score_block(c, d_cache, n + q + i - 1, n_cap, d_tokens, 1, nullptr, nullptr, d_tokens + n + q + i, s);
     return st;
+}
+
+kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int32_t n_cap,
+                                 const int32_t *d_tokens_new, int32_t edit_start, int32_t edit_end, int32_t K,
+                                 int32_t layer, int32_t *d_out, float *d_dev_out, int32_t *n_out, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_select_cacheblend: NULL context");
+    if (!d_cache || !d_tokens_new || !n_out || K < 0 || (K > 0 && !d_out))
+        return fail(c, KVR_E_ARG, "kvr_select_cacheblend: NULL argument or negative K");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_select_cacheblend: cache must be 16-byte aligned");
+    if (n < 1 || n > n_cap || n_cap > c->d.max_ctx || edit_start < 0 || edit_start > edit_end || edit_end > n)
+        return fail(c, KVR_E_RANGE, "kvr_select_cacheblend: need 1 <= n <= n_cap <= max_ctx and "
+                                    "0 <= edit_start <= edit_end <= n");
+    if (layer < 0 || layer >= c->d.n_layers) return fail(c, KVR_E_RANGE, "kvr_select_cacheblend: layer out of range");
+    const int m = std::max(0, n - 1 - edit_end);  // pool D = [edit_end, n - 1)
+    *n_out = std::min(K, m);
+    if (m == 0) return KVR_OK;
+    DeviceGuard g(c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const kvr_dims &d = c->d;
+    const size_t row = (size_t)d.head_dim * elem_size(d);
+    const size_t cache_bytes = align_up((size_t)(layer + 1) * 2 * d.n_kv_heads * n_cap * row, 256);
+    const size_t need = cache_bytes + (size_t)n_cap * 4;
+    if (need > c->sel_bytes) {
+        if (c->sel_scratch) {
+            hipError_t e = hipStreamSynchronize(s);
+            if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: hipStreamSynchronize");
+            (void)hipFree(c->sel_scratch);
+            c->sel_scratch = nullptr;
+            c->sel_bytes = 0;
+        }
+        if (hipMalloc((void **)&c->sel_scratch, need) != hipSuccess)
+            return fail(c, KVR_E_NOMEM, "kvr_select_cacheblend: scratch allocation failed");
+        c->sel_bytes = need;
+    }
+    char *scratch = c->sel_scratch;
+    float *dev = d_dev_out ? d_dev_out : (float *)(scratch + cache_bytes);
+    // layers below `layer`, positions before the edit: the stale states (the
+    // edit does not reach them) for the suffix forward to attend over
+    if (layer > 0 && edit_start > 0) {
+        hipError_t e = hipMemcpy2DAsync(scratch, (size_t)n_cap * row, d_cache, (size_t)n_cap * row,
+                                        (size_t)edit_start * row, (size_t)layer * 2 * d.n_kv_heads,
+                                        hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: hipMemcpy2DAsync");
+    }
+    // the suffix [edit_start, n) of C' through layers 0..layer-1 and the
+    // key/value projection of `layer`, into the scratch cache
+    for (int c0 = edit_start; c0 < n; c0 += c->rows_cap) {
+        const int c1 = std::min(n, c0 + c->rows_cap);
+        Tables t;
+        t.docs.push_back(DocInfo{scratch, d_tokens_new, nullptr, n, n_cap, 0, c1 - c0});
+        t.rows.reserve(c1 - c0);
+        for (int p = c0; p < c1; ++p) t.rows.push_back(RowInfo{p, 0, p - c0, 0});
+        kvr_status st = run_pass(c, t, s, layer);
+        if (st != KVR_OK) return st;
+    }
+    hipError_t e = launch_kv_deviation(c->bf16, scratch, n_cap, layer, d_cache, n_cap, layer, d.n_kv_heads,
+                                       d.head_dim, edit_end, n - 1, dev, s);
+    if (e == hipSuccess) e = launch_topk(dev, m, *n_out, edit_end, d_out, s);
+    if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: deviation / top-K");
+    return KVR_OK;
 }
 
 kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {
