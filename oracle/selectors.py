@@ -2,6 +2,18 @@
 
 TEST INFRASTRUCTURE ONLY; float64; shares no code with the library.
 
+Attention (Table 1: "top-K by stale-cache attention from the query"; Section
+3, "Cost accounting": a stale-cache scoring pass).  Readings (the paper's
+appendix with the aggregation rule is not available):
+* the query tokens are appended after the n stale positions and run through
+  the decoder as in the scoring forward (they attend over the stale cache and
+  causally over each other; their keys/values occupy scratch slots);
+* the score of a stale position p is the softmax attention probability that
+  the query assigns to p, summed over every layer, query head and query
+  token;
+* top-K over the pool D by decreasing score, ties to the lower position,
+  ascending.
+
 CacheBlend (Table 1: "top-K by layer-2 key/value deviation"; Section 3, "Cost
 accounting": it adds roughly one prefill layer over the prefix).  Readings:
 * "layer 2" counts from one, i.e. layer index 1: its keys/values need the
@@ -74,3 +86,42 @@ def select_cacheblend(shape, weights, cache: np.ndarray, tokens_new: np.ndarray,
     check_span(len(tokens_new), edit_start, edit_end, k)
     dev = cacheblend_deviation(shape, weights, cache, tokens_new, edit_start, edit_end, layer)
     return top_k_positions(dev, edit_end, k)
+
+
+def attention_mass(shape, weights, cache: np.ndarray, tokens: np.ndarray, n: int, q: int) -> np.ndarray:
+    """Summed attention probability on each stale position [0, n) from the q
+    query tokens tokens[n:n+q] over all layers and query heads."""
+    tokens = np.asarray(tokens, dtype=np.int64)
+    P = np.arange(n, n + q, dtype=np.int64)
+    scratch = np.array(cache, dtype=np.float64)
+    Hq, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
+    G = Hq // Hkv
+    mass = np.zeros(n, dtype=np.float64)
+    h = weights.embed_rows(tokens[P])
+    for l in range(shape.n_layers):
+        w = weights.layer(l)
+        x = od.rms_norm(h, w["attn_norm"], shape.rms_eps)
+        qx, kx, vx = x @ w["wq"].T, x @ w["wk"].T, x @ w["wv"].T
+        if w.get("bq") is not None:
+            qx, kx, vx = qx + w["bq"], kx + w["bk"], vx + w["bv"]
+        qr = od.rope(qx.reshape(q, Hq, hd), P, shape.rope_theta)
+        kr = od.rope(kx.reshape(q, Hkv, hd), P, shape.rope_theta)
+        scratch[l, 0][:, P, :] = kr.transpose(1, 0, 2)
+        scratch[l, 1][:, P, :] = vx.reshape(q, Hkv, hd).transpose(1, 0, 2)
+        for r in range(q):
+            keys = scratch[l, 0][:, :P[r] + 1, :]
+            for j in range(Hq):
+                sc = keys[j // G] @ qr[r, j] / np.sqrt(hd)
+                pr = np.exp(sc - sc.max())
+                pr /= pr.sum()
+                mass += pr[:n]
+        h = od.layer_forward(shape, w, h, P, scratch[l, 0], scratch[l, 1])
+    return mass
+
+
+def select_attention(shape, weights, cache: np.ndarray, tokens: np.ndarray, n: int, q: int, edit_start: int,
+                     edit_end: int, k: int) -> List[int]:
+    check_span(n, edit_start, edit_end, k)
+    mass = attention_mass(shape, weights, cache, tokens, n, q)
+    D = pool(n, edit_end)
+    return top_k_positions(mass[D[0]:D[-1] + 1] if D else np.zeros(0), edit_end, k)

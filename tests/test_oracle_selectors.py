@@ -69,3 +69,37 @@ def test_top_k_rule_against_exhaustive_search():
         best = max(itertools.combinations(range(m), k),
                    key=lambda c: (sum(dev[list(c)]), [-i for i in sorted(c)]))
         assert osl.top_k_positions(dev, 100, k) == sorted(100 + i for i in best)
+
+
+def test_attention_mass_matches_causal_lm_attentions():
+    """The summed attention on each stale position equals the sum of a float64
+    transformers causal LM's attention probabilities (output_attentions) over
+    layers, heads and query rows, when the stale cache is K(C)."""
+    from tests.test_oracle_scoring import _causal_lm
+    shape = SMALL
+    n, q = 22, 5
+    W, _ = dense(shape, seed=41, std=0.2)
+    lm = synth.make_lm_head(shape, dtype=torch.float32, seed=41).to(torch.float64).numpy()
+    toks = synth.make_tokens(n + q, shape.vocab, seed=42).numpy().astype(np.int64)
+    cache, _ = od.prefill(shape, W, toks[:n], n_cap=n + q)
+    mass = osl.attention_mass(shape, W, cache, toks, n, q)
+    model = _causal_lm(shape, W, lm)
+    with torch.no_grad():
+        att = model(input_ids=torch.from_numpy(toks)[None], output_attentions=True).attentions
+    ref = sum(a[0, :, n:n + q, :n].sum(dim=(0, 1)).numpy() for a in att)
+    assert relmax(mass, ref) < 1e-5
+    # each (layer, head, query row) distributes mass 1 over [0, its position]
+    assert np.sum(mass) <= shape.n_layers * shape.n_heads * q + 1e-9
+
+
+def test_select_attention_takes_top_mass():
+    shape = MICRO_BIAS
+    n, q = 18, 3
+    W, _ = dense(shape, seed=43, std=0.3)
+    toks = synth.make_tokens(n + q, shape.vocab, seed=44).numpy().astype(np.int64)
+    cache, _ = od.prefill(shape, W, toks[:n], n_cap=n + q)
+    mass = osl.attention_mass(shape, W, cache.copy(), toks, n, q)
+    sel = osl.select_attention(shape, W, cache.copy(), toks, n, q, 4, 6, 5)
+    assert len(sel) == 5 and all(6 <= p < n - 1 for p in sel)
+    rest = [p for p in range(6, n - 1) if p not in sel]
+    assert min(mass[sel]) >= max(mass[rest])
