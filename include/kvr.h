@@ -221,6 +221,30 @@ kvr_status kvr_select_cacheblend(kvr_ctx *ctx, const void *d_cache, int32_t n, i
                                  const int32_t *d_tokens_new, int32_t edit_start, int32_t edit_end, int32_t K,
                                  int32_t layer, int32_t *d_out, float *d_dev_out, int32_t *n_out, void *stream);
 
+/* Attention selector (Table 1: top-K by the query's attention over the stale
+ * cache; Section 3, "Cost accounting": one stale-cache scoring pass).  Runs
+ * the q query tokens d_tokens[n .. n+q) after the n stale positions of
+ * d_cache, as kvr_score does (they attend over the stale cache and causally
+ * over each other; their keys/values land in cache slots [n, n+q), which are
+ * scratch; rows [0, n) are only read), and accumulates for every stale
+ * position p < n
+ *   mass[p] = sum over layers, query heads and query tokens of the softmax
+ *             probability that the token places on p
+ * (the aggregation rule is a reading: the paper does not state it).  Writes to
+ * d_out (device, K entries) the min(K, |D|) positions of the pool
+ * D = [edit_end, n - 1) with the largest mass (ties: lower position) in
+ * ascending order; *n_out (host) receives that count.  d_mass_out (device,
+ * n floats, or NULL) receives mass[0 .. n).  d_tokens must hold n + q ids
+ * (only the query's are read).  The last layer's output projection and MLP
+ * are not run: the mass is complete after its attention.
+ * Errors: KVR_E_ARG (NULL argument, negative K, misaligned cache),
+ * KVR_E_RANGE (need 1 <= n, 1 <= q <= the context's rows per pass,
+ * n + q <= n_cap <= max_ctx, 0 <= edit_start <= edit_end <= n),
+ * KVR_E_NOMEM, KVR_E_HIP. */
+kvr_status kvr_select_attention(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens,
+                                int32_t q, int32_t edit_start, int32_t edit_end, int32_t K, int32_t *d_out,
+                                float *d_mass_out, int32_t *n_out, void *stream);
+
 /* EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"): the
  * structural variant that recomputes from the end of the edit to the next
  * document boundary, with no selector forward.  Returns the positions

@@ -23,6 +23,8 @@
 // as a compensated pair.  When the key range of a row block is split over
 // several items (few rows, long contexts) each item writes (m, l, unnormalised
 // O) partials and a combine pass merges them with log-sum-exp rescaling.
+// When `lse` is given, the row's softmax normaliser is also written there:
+// lse[r * Hq + j] = log2 of the sum over its keys of 2^(q.k * log2(e)/sqrt(hd)).
 #include <math.h>
 
 #include <algorithm>
@@ -63,7 +65,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                                                                     const RowInfo *rows, const DocInfo *docs,
                                                                     const AttnItem *items, int layer, int Hq, int Hkv,
                                                                     int MT, float *part, bf16_t *O, bf16_t *O_lo,
-                                                                    int o_perm) {
+                                                                    int o_perm, float *lse) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS_STRIDE];
     __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * VT_STRIDE];
 
@@ -266,6 +268,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 *reinterpret_cast<uint2 *>(O + off) = make_uint2(hi[0], hi[1]);
                 *reinterpret_cast<uint2 *>(O_lo + off) = make_uint2(lo[0], lo[1]);
             }
+            if (lse && g == 0) lse[(size_t)r * Hq + j] = m[i] + log2f(l[i]);
         } else {
             float *p = part + ((size_t)(it.part * G + t) * rows_item + ri) * PART_ROW;
 #pragma unroll
@@ -279,9 +282,10 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
 // head dimension: merge the split partials of one row with log-sum-exp
 // weights (exp2 domain).  The maximum over the parts is taken first so that
 // every part's loads are independent of the others' (batches of eight loads in
-// flight); the parts are then summed in ascending order.
+// flight); the parts are then summed in ascending order.  `lse` as above.
 __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
-                                                                int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm) {
+                                                                int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm,
+                                                                float *lse) {
     constexpr int B = 8;
     const CombineItem it = items[blockIdx.x];
     const int t = blockIdx.y, i = blockIdx.z;
@@ -330,6 +334,7 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
     }
     const int r = it.row0 + i, c = j * HD + d;
     store_operand(O, O_lo, o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c, acc / L);
+    if (lse && d == 0) lse[(size_t)r * Hq + j] = M + log2f(L);
 }
 
 }  // namespace
@@ -341,28 +346,28 @@ int attention_row_tiles(int Hq, int Hkv) {
 
 hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O,
-                                 bf16_t *O_lo, bool o_perm, hipStream_t s) {
+                                 bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     if (!Q_lo || !O_lo) return hipErrorInvalidValue;
     const int MT = attention_row_tiles(Hq, Hkv);
     const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
     if (ppw == 1)
         kvr_launch(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
-                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
+                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
     else if (ppw == 2)
         kvr_launch(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
-                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm);
+                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq, int Hkv,
-                                    bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s) {
+                                    bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     const int MT = attention_row_tiles(Hq, Hkv);
     kvr_launch(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
-                       Hkv, MT, O, O_lo, (int)o_perm);
+                       Hkv, MT, O, O_lo, (int)o_perm, lse);
     return hipGetLastError();
 }
 

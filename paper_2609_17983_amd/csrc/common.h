@@ -165,18 +165,21 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
                                const void *bv, const RowInfo *rows, const DocInfo *docs, int R, int layer, int Hq,
                                int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q, void *Q_lo,
                                hipStream_t s);
-// O is written row-major [R][Hq*hd], or in operand order when o_perm.
+// O is written row-major [R][Hq*hd], or in operand order when o_perm.  The
+// attention launchers also write, when lse is not null, each (row, query head)
+// softmax normaliser as a base-2 log-sum-exp of the scores q.k*log2(e)/sqrt(hd):
+// lse[r * Hq + j].
 hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, const RowInfo *rows,
                                    const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd, void *O, void *O_lo,
-                                   bool o_perm, hipStream_t s);
+                                   bool o_perm, float *lse, hipStream_t s);
 // 16-row tiles per attention work item for a head grouping (items carry up to
 // 16 * this many rows).
 int attention_row_tiles(int Hq, int Hkv);
 hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
-                                 float *part, bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s);
+                                 float *part, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s);
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
-                                    int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, hipStream_t s);
+                                    int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s);
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
 // Skinny MFMA path (R <= 64); nt = 16-row weight tiles per block (1..8).
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s);
@@ -202,6 +205,16 @@ hipError_t launch_logsoftmax(const float *part, int nsplit, int R, int V, const 
 // layouts with their own n_cap), p in [p0, p1).
 hipError_t launch_kv_deviation(bool bf16, const void *fresh, int fresh_ncap, int fl, const void *stale, int stale_ncap,
                                int sl, int Hkv, int hd, int p0, int p1, float *dev, hipStream_t s);
+// Attention selector, one layer: part[g * n + p] (=, or += when accumulate)
+// the attention probability that the q query rows (row-major Q [q][Hq*hd],
+// compensated pair in bf16; lse from the same layer's attention launch) place
+// on stale key p < n of kv head g, summed over the rows and the group's heads.
+bool attn_mass_mfma_ok(bool bf16, int hd);
+hipError_t launch_attn_mass(bool bf16, const void *Q, const void *Q_lo, const float *lse, int q, const void *cache,
+                            int n_cap, int layer, int Hq, int Hkv, int hd, int n, float *part, bool accumulate,
+                            hipStream_t s);
+// mass[p] = sum over g of part[g * n + p], p < n.
+hipError_t launch_mass_reduce(const float *part, int Hkv, int n, float *mass, hipStream_t s);
 // The K largest of dev[0, m) (ties: lower index), as ascending positions p0 + i.
 hipError_t launch_topk(const float *dev, int m, int K, int p0, int32_t *out, hipStream_t s);
 

@@ -52,7 +52,7 @@ struct kvr_ctx {
     const void *lm_head = nullptr;
     void *lm_pk = nullptr;
     size_t lm_pk_bytes = 0;
-    char *sel_scratch = nullptr;  // CacheBlend: fresh keys/values of the first layers + deviations
+    char *sel_scratch = nullptr;  // selectors: CacheBlend fresh keys/values + deviations; Attention mass
     size_t sel_bytes = 0;
     float *score_y = nullptr;     // hidden rows of the scored block [max rows][d]
     float *score_part = nullptr;  // logit tiles [split][64][vocab]
@@ -98,11 +98,11 @@ constexpr int SPLIT_MAX = 32;
 
 enum Step {
     ST_EMBED, ST_NORM, ST_QKV, ST_ROPE, ST_ATTN, ST_COMBINE, ST_OPROJ, ST_GATEUP, ST_DOWN, ST_FINAL, ST_LMHEAD,
-    ST_LOGSOFTMAX, ST_COUNT
+    ST_LOGSOFTMAX, ST_MASS, ST_COUNT
 };
 const char *const STEP_NAMES[ST_COUNT] = {"embed", "rmsnorm", "qkv_proj", "rope_scatter", "attention",
                                           "attention_combine", "o_proj", "gate_up_swiglu", "down_proj", "final_norm",
-                                          "lm_head", "logsoftmax"};
+                                          "lm_head", "logsoftmax", "attention_mass"};
 constexpr int SCORE_ROWS = 64;  // rows per LM-head launch (the skinny kernel's bound)
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -290,10 +290,21 @@ void disarm(kvr_ctx *c, int step, hipEvent_t start, hipEvent_t stop) {
     }
 }
 
+// Attention-mass accumulation during a pass of query rows (Attention
+// selector): after each layer's attention the probability mass the pass's
+// rows place on the stale keys [0, n) is added to part [Hkv][n]; the pass ends
+// after the last layer's attention.
+struct MassHook {
+    const void *cache;
+    int n_cap, n;
+    float *lse;   // [rows][Hq]
+    float *part;  // [Hkv][n]
+};
+
 // Upload the tables of a pass and enqueue its kernels.  kv_layer >= 0 stops
 // the pass at that layer once its fresh keys/values are in the cache (layers
 // below it run in full; no final norm).
-kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1) {
+kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, const MassHook *mh = nullptr) {
     const kvr_dims &d = c->d;
     const int R = (int)t.rows.size();
     if (R == 0) return KVR_OK;
@@ -368,18 +379,25 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1) {
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
                                       hd, c->rope_cos, c->rope_sin, c->Qb, c->Qb_lo, s), "rope_scatter", ST_ROPE);
         if (l == kv_layer) return KVR_OK;
+        float *lse = mh ? mh->lse : nullptr;
         if (attn_mfma) {
             KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, docs, items,
                                             (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
-                                            (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, s),
+                                            (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, lse, s),
                       "attention", ST_ATTN);
             if (!t.comb.empty())
                 KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
-                                                   (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, s), "attention_combine", ST_COMBINE);
+                                                   (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, lse, s), "attention_combine", ST_COMBINE);
         } else {
             KVR_CHECK(launch_attention_simple(bf, c->Qb, c->Qb_lo, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob,
-                                              c->Ob_lo, sk, s),
+                                              c->Ob_lo, sk, lse, s),
                       "attention_simple", ST_ATTN);
+        }
+        if (mh) {
+            KVR_CHECK(launch_attn_mass(bf, c->Qb, c->Qb_lo, mh->lse, R, mh->cache, mh->n_cap, l, d.n_heads,
+                                       d.n_kv_heads, hd, mh->n, mh->part, l > 0, s),
+                      "attention_mass", ST_MASS);
+            if (l == d.n_layers - 1) return KVR_OK;
         }
         if (sk) {
             KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
@@ -771,6 +789,23 @@ kvr_status kvr_generate(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, int
     return st;
 }
 
+// Grow the selectors' scratch to at least `need` bytes (waits for the stream
+// before freeing the old buffer).
+static kvr_status sel_reserve(kvr_ctx *c, size_t need, hipStream_t s, const char *who) {
+    if (need <= c->sel_bytes) return KVR_OK;
+    if (c->sel_scratch) {
+        hipError_t e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(c, e, (std::string(who) + ": hipStreamSynchronize").c_str());
+        (void)hipFree(c->sel_scratch);
+        c->sel_scratch = nullptr;
+        c->sel_bytes = 0;
+    }
+    if (hipMalloc((void **)&c->sel_scratch, need) != hipSuccess)
+        return fail(c, KVR_E_NOMEM, std::string(who) + ": scratch allocation failed");
+    c->sel_bytes = need;
+    return KVR_OK;
+}
+
 kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int32_t n_cap,
                                  const int32_t *d_tokens_new, int32_t edit_start, int32_t edit_end, int32_t K,
                                  int32_t layer, int32_t *d_out, float *d_dev_out, int32_t *n_out, void *stream) {
@@ -790,19 +825,8 @@ kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int
     const kvr_dims &d = c->d;
     const size_t row = (size_t)d.head_dim * elem_size(d);
     const size_t cache_bytes = align_up((size_t)(layer + 1) * 2 * d.n_kv_heads * n_cap * row, 256);
-    const size_t need = cache_bytes + (size_t)n_cap * 4;
-    if (need > c->sel_bytes) {
-        if (c->sel_scratch) {
-            hipError_t e = hipStreamSynchronize(s);
-            if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: hipStreamSynchronize");
-            (void)hipFree(c->sel_scratch);
-            c->sel_scratch = nullptr;
-            c->sel_bytes = 0;
-        }
-        if (hipMalloc((void **)&c->sel_scratch, need) != hipSuccess)
-            return fail(c, KVR_E_NOMEM, "kvr_select_cacheblend: scratch allocation failed");
-        c->sel_bytes = need;
-    }
+    kvr_status st0 = sel_reserve(c, cache_bytes + (size_t)n_cap * 4, s, "kvr_select_cacheblend");
+    if (st0 != KVR_OK) return st0;
     char *scratch = c->sel_scratch;
     float *dev = d_dev_out ? d_dev_out : (float *)(scratch + cache_bytes);
     // layers below `layer`, positions before the edit: the stale states (the
@@ -828,6 +852,44 @@ kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int
                                        d.head_dim, edit_end, n - 1, dev, s);
     if (e == hipSuccess) e = launch_topk(dev, m, *n_out, edit_end, d_out, s);
     if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: deviation / top-K");
+    return KVR_OK;
+}
+
+kvr_status kvr_select_attention(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens,
+                                int32_t q, int32_t edit_start, int32_t edit_end, int32_t K, int32_t *d_out,
+                                float *d_mass_out, int32_t *n_out, void *stream) {
+    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_select_attention: NULL context");
+    if (!d_cache || !d_tokens || !n_out || K < 0 || (K > 0 && !d_out))
+        return fail(c, KVR_E_ARG, "kvr_select_attention: NULL argument or negative K");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_select_attention: cache must be 16-byte aligned");
+    if (n < 1 || q < 1 || (long long)n + q > n_cap || n_cap > c->d.max_ctx || edit_start < 0 ||
+        edit_start > edit_end || edit_end > n)
+        return fail(c, KVR_E_RANGE, "kvr_select_attention: need 1 <= n, 1 <= q, n + q <= n_cap <= max_ctx and "
+                                    "0 <= edit_start <= edit_end <= n");
+    if (q > c->rows_cap) return fail(c, KVR_E_RANGE, "kvr_select_attention: query longer than one pass holds");
+    const int m = std::max(0, n - 1 - edit_end);  // pool D = [edit_end, n - 1)
+    *n_out = std::min(K, m);
+    if (m == 0 && !d_mass_out) return KVR_OK;
+    DeviceGuard g(c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const kvr_dims &d = c->d;
+    const size_t part_bytes = align_up((size_t)d.n_kv_heads * n * 4, 256);
+    const size_t lse_bytes = align_up((size_t)q * d.n_heads * 4, 256);
+    kvr_status st = sel_reserve(c, part_bytes + lse_bytes + (size_t)n * 4, s, "kvr_select_attention");
+    if (st != KVR_OK) return st;
+    MassHook mh{d_cache, n_cap, n, (float *)(c->sel_scratch + part_bytes), (float *)c->sel_scratch};
+    float *mass = d_mass_out ? d_mass_out : (float *)(c->sel_scratch + part_bytes + lse_bytes);
+    // the query rows at positions [n, n + q) over the stale cache (their own
+    // keys/values land in slots [n, n + q))
+    Tables t;
+    t.docs.push_back(DocInfo{d_cache, d_tokens, nullptr, n + q, n_cap, 0, q});
+    t.rows.reserve(q);
+    for (int j = 0; j < q; ++j) t.rows.push_back(RowInfo{n + j, 0, j, 0});
+    st = run_pass(c, t, s, -1, &mh);
+    if (st != KVR_OK) return st;
+    hipError_t e = launch_mass_reduce(mh.part, d.n_kv_heads, n, mass, s);
+    if (e == hipSuccess && m > 0) e = launch_topk(mass + edit_end, m, *n_out, edit_end, d_out, s);
+    if (e != hipSuccess) return hip_fail(c, e, "kvr_select_attention: reduce / top-K");
     return KVR_OK;
 }
 

@@ -226,10 +226,12 @@ __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, in
 }
 
 // One wavefront per (row, query head): online softmax over keys 0..pos.
+// When `lse` is given, lse[r * Hq + j] = log2 of the softmax normaliser of the
+// scores q.k * log2(e)/sqrt(hd) (the base-2 log-sum-exp).
 template <typename T>
 __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const T *Q_lo, const RowInfo *rows,
                                                               const DocInfo *docs, int layer, int Hq, int Hkv, int hd,
-                                                              T *O, T *O_lo, int o_perm) {
+                                                              T *O, T *O_lo, int o_perm, float *lse) {
     const int r = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
     const RowInfo ri = rows[r];
     const DocInfo dc = docs[ri.doc];
@@ -261,6 +263,7 @@ __global__ __launch_bounds__(64) void attention_simple_kernel(const T *Q, const 
     if (has1)
         store_operand(O, O_lo, o_perm ? perm_offset(r, j * hd + lane + 64, qd) : (size_t)r * qd + j * hd + lane + 64,
                       a1 * inv);
+    if (lse && lane == 0) lse[(size_t)r * Hq + j] = (m + logf(l)) * 1.4426950408889634f;
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
@@ -413,14 +416,14 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
 
 hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, const RowInfo *rows,
                                    const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd, void *O, void *O_lo,
-                                   bool o_perm, hipStream_t s) {
+                                   bool o_perm, float *lse, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (bf16)
         kvr_launch(attention_simple_kernel<bf16_t>, dim3(R, Hq), dim3(64), 0, s, (const bf16_t *)Q,
-                           (const bf16_t *)Q_lo, rows, docs, layer, Hq, Hkv, hd, (bf16_t *)O, (bf16_t *)O_lo, (int)o_perm);
+                           (const bf16_t *)Q_lo, rows, docs, layer, Hq, Hkv, hd, (bf16_t *)O, (bf16_t *)O_lo, (int)o_perm, lse);
     else if (!o_perm)
         kvr_launch(attention_simple_kernel<float>, dim3(R, Hq), dim3(64), 0, s, (const float *)Q,
-                           (const float *)nullptr, rows, docs, layer, Hq, Hkv, hd, (float *)O, (float *)nullptr, 0);
+                           (const float *)nullptr, rows, docs, layer, Hq, Hkv, hd, (float *)O, (float *)nullptr, 0, lse);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

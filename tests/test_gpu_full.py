@@ -26,6 +26,7 @@ import paper_2609_17983_amd as kvr
 import synth
 from oracle import decoder as od
 from oracle import select as osel
+from oracle import selectors as osl
 from tests.gpu_util import TOL, Engine, OracleWeights, compare_repair, relmax, say
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
@@ -116,6 +117,38 @@ def test_llama8b_endpoint_property(llama):
     e_h = relmax(h_rep.cpu().numpy(), h_pre.cpu().numpy())
     say(f"llama8b endpoint: cache {e_cache:.3e} hidden {e_h:.3e}")
     assert e_cache <= TOL[kvr.KVR_BF16] and e_h <= TOL[kvr.KVR_BF16]
+
+
+def test_llama8b_attention_selector(llama):
+    """Attention selector at full size: a 16-token query over a 5000-position
+    synthetic stale cache; the per-position mass is compared with the oracle
+    in full, the selection where it is decided by a clear gap."""
+    shape = llama.shape
+    q, K = 16, 32
+    e = synth.edit_position(1000, 4000, label=5)
+    toks = synth.make_tokens(N + q, shape.vocab, seed=21)
+    cache = synth.make_stale_cache(shape, N + q, device="cuda", label=21)
+    ref_in = cache.to(torch.float64).cpu().numpy()
+    out = torch.full((K,), -1, dtype=torch.int32, device="cuda")
+    mass = torch.empty(N, device="cuda")
+    say(f"llama8b attention selector n={N} q={q} edit@{e}")
+    cnt = kvr.kvr_select_attention(llama.ctx, cache.data_ptr(), N, N + q, toks.cuda().data_ptr(), q, e, e + SPAN, K,
+                                   out.data_ptr(), mass.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert cnt == K
+    say("llama8b attention selector: oracle mass")
+    ref = osl.attention_mass(shape, OracleWeights(llama.weights), ref_in, toks.numpy(), N, q)
+    got = mass.cpu().numpy().astype(np.float64)
+    err = relmax(got, ref)
+    say(f"llama8b attention selector: mass err {err:.3e}")
+    assert err <= TOL[kvr.KVR_BF16]
+    sel = out.cpu().tolist()
+    D0 = e + SPAN
+    assert sel == osl.top_k_positions(got[D0:N - 1], D0, K)
+    srt = np.sort(ref[D0:N - 1])[::-1]
+    band = 2 * TOL[kvr.KVR_BF16] * np.max(ref)
+    sure = {D0 + i for i in range(N - 1 - D0) if ref[D0 + i] > srt[K - 1] + band}
+    assert sure <= set(sel)
 
 
 def test_llama8b_batched_64_docs(llama):
