@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device-to-device copy first (reference for HBM byte counters)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-adjacent", action="store_true",
+                    help="skip the timings of the scoring forward, the selectors and transplant")
     return ap.parse_args()
 
 
@@ -143,7 +145,7 @@ def main():
         log("calibration copy: 1 GiB read + 1 GiB written")
         del src, dst
     w = synth.make_weights(shape, dtype=torch.bfloat16, device="cuda")
-    dims = kvr.dims_for(shape, kvr.KVR_BF16, max_ctx=n_max, max_rows=max(R, 64))
+    dims = kvr.dims_for(shape, kvr.KVR_BF16, max_ctx=n_max + ADJ_SLOTS, max_rows=max(R, 64))
     ctx = kvr.kvr_create(dims, kvr.weights_struct(w))
 
     # stale caches K(C) by the engine's own prefill, then the edited ids C'
@@ -271,6 +273,11 @@ def main():
         n0, e0, A0 = plans[0]
         cpu = cpu_baseline(shape, w, n0, e0, span, A0, min(args.cpu_layers, L), len(plans), torch)
 
+    adj = None
+    if not batched and not args.no_adjacent:
+        adj = adjacent_rows(kvr, synth, torch, ctx, shape, plans[0], olds[0], news[0], caches[0], span, stream,
+                            max(3, args.steps // 4))
+
     rbytes = repair_bytes(shape, plans, span)
     rflops = repair_flops(shape, plans, span)
     if batched:
@@ -321,8 +328,119 @@ def main():
         out["per_seed_ms"] = per_seed
         out["per_seed_edits"] = seed_edits
         out["median_over_seeds_ms"] = round(statistics.median(per_seed), 4)
+    if adj is not None:
+        out["adjacent_rows"] = adj
     print(json.dumps(out), flush=True)
     kvr.kvr_destroy(ctx)
+
+
+ADJ_SLOTS = 64     # cache slots past the context for appended query/answer tokens
+ADJ_QUERY = 16     # query tokens of the scoring forward and the Attention selector
+ADJ_ANSWER = 8     # answer tokens scored after the query
+ADJ_GEN = 16       # greedy tokens generated (the flip test's continuation length)
+
+
+def adjacent_rows(kvr, synth, torch, ctx, shape, plan, old, new, cache, span, stream, reps):
+    """Times the steps around the repair on the same workload: the fresh-query
+    scoring forward (query + answer teacher-forced, and a greedy continuation),
+    the CacheBlend and Attention selectors, transplant of the repaired set, and
+    the host selectors.  Each is enqueued `reps` times after two warmup calls
+    and timed with HIP events on the stream the kernels run on."""
+    n, e, A = plan
+    L, es = shape.n_layers, 2
+    dev = cache.device
+    ncap = n + ADJ_SLOTS
+    kvpos = shape.kv_bytes_per_pos(es)
+    wbytes = L * shape.layer_params() * es
+    lm_bytes = shape.vocab * shape.d_model * es
+    # a cache with room for appended tokens: the repaired cache's rows [0, n)
+    work = torch.empty((L, 2, shape.n_kv_heads, ncap, shape.head_dim), dtype=torch.bfloat16, device=dev)
+    work[:, :, :, :n].copy_(cache)
+    q_ids = synth.make_tokens(ADJ_QUERY + ADJ_ANSWER, shape.vocab, seed=77).to(dev)
+    toks = torch.cat([new.to(dev), q_ids, torch.zeros(ADJ_SLOTS, dtype=torch.int32, device=dev)])
+    s = stream.cuda_stream
+
+    def time_it(fn):
+        for _ in range(2):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(reps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    out = {}
+    m = ADJ_QUERY + ADJ_ANSWER
+    lp = torch.empty(m, dtype=torch.float32, device=dev)
+    am = torch.empty(m, dtype=torch.int32, device=dev)
+    t = time_it(lambda: kvr.kvr_score(ctx, work.data_ptr(), n, ncap, toks.data_ptr(), m, lp.data_ptr(), am.data_ptr(), s))
+    b = wbytes + lm_bytes + (n + m) * kvpos
+    out["score"] = {"what": f"kvr_score: {ADJ_QUERY}-token query + {ADJ_ANSWER}-token answer after the {n}-token "
+                            f"cache, teacher-forced log-probs and argmax", "ms": round(t, 4),
+                    "algorithmic_bytes": b, "hbm_gb_s": round(b / (t * 1e-3) / 1e9, 1)}
+    gtoks = toks.clone()
+    t = time_it(lambda: kvr.kvr_generate(ctx, work.data_ptr(), n, ncap, gtoks.data_ptr(), ADJ_QUERY, ADJ_GEN, s))
+    b = ADJ_GEN * (wbytes + lm_bytes) + ADJ_GEN * (n + ADJ_QUERY + ADJ_GEN) * kvpos
+    out["generate"] = {"what": f"kvr_generate: {ADJ_QUERY}-token query then {ADJ_GEN} greedy tokens",
+                       "ms": round(t, 4), "ms_per_token": round(t / ADJ_GEN, 4), "algorithmic_bytes": b,
+                       "hbm_gb_s": round(b / (t * 1e-3) / 1e9, 1)}
+
+    K = len(A)
+    sel = torch.empty(max(K, 1), dtype=torch.int32, device=dev)
+    # CacheBlend: layer 0 and the key/value projection of layer 1 over the
+    # suffix [e, n) of C' (an MFMA-bound partial prefill), deviation, top-K
+    t = time_it(lambda: kvr.kvr_select_cacheblend(ctx, cache.data_ptr(), n, n, new.data_ptr(), e, e + span, K, 1,
+                                                  sel.data_ptr(), None, s))
+    rows = n - e
+    d, f = shape.d_model, shape.d_ffn
+    fl = 2 * rows * (shape.layer_params() + d * 2 * shape.kv_dim) + 4 * shape.n_heads * shape.head_dim * \
+        sum(p + 1 for p in range(e, n))
+    out["select_cacheblend"] = {"what": f"kvr_select_cacheblend layer 1 (the paper's layer 2): {rows} suffix rows",
+                                "ms": round(t, 4), "algorithmic_flops": fl,
+                                "mfma_tflops": round(fl / (t * 1e-3) / 1e12, 1)}
+    mass = torch.empty(n, dtype=torch.float32, device=dev)
+    def attn_sel():
+        kvr.kvr_select_attention(ctx, work.data_ptr(), n, ncap, toks.data_ptr(), ADJ_QUERY, e, e + span, K,
+                                 sel.data_ptr(), mass.data_ptr(), s)
+
+    t = time_it(attn_sel)
+    # kernel times from a separate loop with the step profiler on
+    kvr.kvr_profile_enable(ctx, True)
+    kvr.kvr_profile_read(ctx)
+    time_it(attn_sel)
+    prof = kvr.kvr_profile_read(ctx)
+    kvr.kvr_profile_enable(ctx, False)
+    b = wbytes + n * kvpos + n * kvpos // 2
+    mass_ms, mass_n = prof.get("attention_mass", (0.0, 0))
+    mass_bytes = n * kvpos // 2  # every stale key read once per layer
+    out["select_attention"] = {
+        "what": f"kvr_select_attention: {ADJ_QUERY}-token query over the {n}-token stale cache, attention mass, top-K",
+        "ms": round(t, 4), "algorithmic_bytes": b, "hbm_gb_s": round(b / (t * 1e-3) / 1e9, 1),
+        "attention_mass_kernel_us": round(mass_ms / max(mass_n, 1) * 1e3, 2),
+        "attention_mass_kernel_gb_s": round(mass_bytes / L / (mass_ms / max(mass_n, 1) * 1e-3) / 1e9, 1)
+        if mass_n else None}
+    P = list(range(e, e + span)) + list(A)
+    pos = sorted(P)
+    t = time_it(lambda: kvr.kvr_transplant(ctx, work.data_ptr(), ncap, cache.data_ptr(), n, pos, s))
+    b = 2 * len(pos) * kvpos
+    out["transplant"] = {"what": f"kvr_transplant of the {len(pos)} repaired positions, every layer and kv head",
+                         "ms": round(t, 4), "algorithmic_bytes": b, "hbm_gb_s": round(b / (t * 1e-3) / 1e9, 1)}
+    import time as _t
+    t0 = _t.perf_counter()
+    for i in range(1000):
+        kvr.kvr_select(kvr.KVR_RANDOM, n, e, e + span, 512, i)
+    # per call through the Python binding (1000 calls: total ms = us per call)
+    out["select_random_k512_host_us"] = round((_t.perf_counter() - t0) * 1e3, 3)
+    t0 = _t.perf_counter()
+    for i in range(1000):
+        kvr.kvr_select_to_boundary(n, e, e + span, min(n - 1, e + span + 64))
+    out["select_to_boundary_host_us"] = round((_t.perf_counter() - t0) * 1e3, 3)
+    log("adjacent rows: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in out.items() if isinstance(v, dict)))
+    del work
+    return out
 
 
 def _kernel_sha():
