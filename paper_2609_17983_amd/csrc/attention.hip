@@ -43,6 +43,7 @@ constexpr int KS_STRIDE = HD + 8;  // keys tile row stride (bf16)
 constexpr int VT_STRIDE = KT + 8;  // transposed values row stride (bf16)
 constexpr int PART_ROW = HD + 4;   // floats per (head, row) partial: O[128], m, l
 constexpr float RESCALE_SLACK = 8.0f;  // log2 headroom before the running max is raised
+constexpr int COMBINE_NP = 16;         // partials per row loaded in one round by the combine
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(2))) float f32x2;
@@ -280,13 +281,14 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
 
 // One block per (combine item, query head of the group, row), one thread per
 // head dimension: merge the split partials of one row with log-sum-exp
-// weights (exp2 domain).  The maximum over the parts is taken first so that
-// every part's loads are independent of the others' (batches of eight loads in
-// flight); the parts are then summed in ascending order.  `lse` as above.
+// weights (exp2 domain), summing the parts in ascending order.  With at most
+// NP parts every partial of the row is loaded in one round (clamped indexes,
+// so the loads are unconditional and all in flight together); longer lists
+// take batches of NP.  `lse` as above.
+template <int NP>
 __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
                                                                 int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm,
                                                                 float *lse) {
-    constexpr int B = 8;
     const CombineItem it = items[blockIdx.x];
     const int t = blockIdx.y, i = blockIdx.z;
     if (i >= it.nrows) return;
@@ -297,40 +299,29 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
     const size_t qstride = (size_t)G * rows_item * PART_ROW;
     const float *base = part + ((size_t)(it.part0 * G + t) * rows_item + i) * PART_ROW;
     const int np = it.nparts;
-    float M = -INFINITY;
-    int q = 0;
-    for (; q + B <= np; q += B) {
-        float mm[B];
+    float M = -INFINITY, acc = 0.f, L = 0.f;
+    for (int q0 = 0; q0 < np; q0 += NP) {
+        float mm[NP], ll[NP], oo[NP];
 #pragma unroll
-        for (int u = 0; u < B; ++u) mm[u] = base[(q + u) * qstride + HD];
-#pragma unroll
-        for (int u = 0; u < B; ++u) M = fmaxf(M, mm[u]);
-    }
-    for (; q < np; ++q) M = fmaxf(M, base[q * qstride + HD]);
-    float acc = 0.f, L = 0.f;
-    q = 0;
-    for (; q + B <= np; q += B) {
-        float mm[B], ll[B], oo[B];
-#pragma unroll
-        for (int u = 0; u < B; ++u) {
-            const float *p = base + (q + u) * qstride;
+        for (int u = 0; u < NP; ++u) {
+            const float *p = base + (size_t)min(q0 + u, np - 1) * qstride;
             mm[u] = p[HD];
             ll[u] = p[HD + 1];
             oo[u] = p[d];
         }
+        float Mb = M;
 #pragma unroll
-        for (int u = 0; u < B; ++u) {
-            const float wq = mm[u] == -INFINITY ? 0.f : exp2f(mm[u] - M);
+        for (int u = 0; u < NP; ++u) Mb = fmaxf(Mb, mm[u]);  // clamped duplicates do not change the max
+        const float r = M == -INFINITY ? 0.f : exp2f(M - Mb);  // rescale what earlier batches summed
+        acc *= r;
+        L *= r;
+#pragma unroll
+        for (int u = 0; u < NP; ++u) {
+            const float wq = (q0 + u >= np || mm[u] == -INFINITY) ? 0.f : exp2f(mm[u] - Mb);
             acc += oo[u] * wq;
             L += ll[u] * wq;
         }
-    }
-    for (; q < np; ++q) {
-        const float *p = base + q * qstride;
-        const float mq = p[HD];
-        const float wq = mq == -INFINITY ? 0.f : exp2f(mq - M);
-        acc += p[d] * wq;
-        L += p[HD + 1] * wq;
+        M = Mb;
     }
     const int r = it.row0 + i, c = j * HD + d;
     store_operand(O, O_lo, o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c, acc / L);
@@ -366,8 +357,8 @@ hipError_t launch_attention_combine(const CombineItem *items, int n_items, const
                                     bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     const int MT = attention_row_tiles(Hq, Hkv);
-    kvr_launch(attention_combine_kernel, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part, Hq,
-                       Hkv, MT, O, O_lo, (int)o_perm, lse);
+    kvr_launch(attention_combine_kernel<COMBINE_NP>, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part,
+               Hq, Hkv, MT, O, O_lo, (int)o_perm, lse);
     return hipGetLastError();
 }
 

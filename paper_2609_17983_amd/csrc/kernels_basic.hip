@@ -26,15 +26,34 @@ __device__ __forceinline__ float block_sum256(float v, float *red) {
     return t;
 }
 
-// Token ids outside [0, vocab) are clamped into range rather than read out of bounds.
+// Token ids outside [0, vocab) are clamped into range rather than read out of
+// bounds.  Rows are copied in 16-byte chunks when d allows it (the table and H
+// are 16-byte aligned).
 template <typename TW>
 __global__ __launch_bounds__(256) void embed_kernel(const RowInfo *rows, const DocInfo *docs, const TW *embed,
                                                     int d, int vocab, float *H) {
+    constexpr int V = 16 / sizeof(TW);  // table elements per chunk
     const int r = blockIdx.x;
     const RowInfo ri = rows[r];
     const int tok = min(max(docs[ri.doc].tokens[ri.pos], 0), vocab - 1);
     const TW *src = embed + (size_t)tok * d;
-    for (int i = threadIdx.x; i < d; i += 256) H[(size_t)r * d + i] = to_f32(src[i]);
+    float *dst = H + (size_t)r * d;
+    if (d % V != 0) {
+        for (int i = threadIdx.x; i < d; i += 256) dst[i] = to_f32(src[i]);
+        return;
+    }
+    for (int i = threadIdx.x; i < d / V; i += 256) {
+        const u32x4 u = *reinterpret_cast<const u32x4 *>(src + (size_t)i * V);
+        if constexpr (sizeof(TW) == 2) {
+            float4 *o = reinterpret_cast<float4 *>(dst + (size_t)i * V);
+            o[0] = make_float4(__uint_as_float(u[0] << 16), __uint_as_float(u[0] & 0xffff0000u),
+                               __uint_as_float(u[1] << 16), __uint_as_float(u[1] & 0xffff0000u));
+            o[1] = make_float4(__uint_as_float(u[2] << 16), __uint_as_float(u[2] & 0xffff0000u),
+                               __uint_as_float(u[3] << 16), __uint_as_float(u[3] & 0xffff0000u));
+        } else {
+            *reinterpret_cast<u32x4 *>(dst + (size_t)i * V) = u;
+        }
+    }
 }
 
 // Sum over a 1024-thread block.
