@@ -198,7 +198,9 @@ hipError_t launch_to_operand(bool bf16, bool perm, const float *Y, int R, int d,
 // lp[r] = log p(target[r]) for r < n_targets, argmax[r] (lowest index among
 // maxima; argmax may be null), next[0] = argmax of row R-1 when next is given.
 hipError_t launch_logsoftmax(const float *part, int nsplit, int R, int V, const int32_t *target, int n_targets,
-                             float *lp, int32_t *argmax, int32_t *next, hipStream_t s);
+                             float *lp, int32_t *argmax, int32_t *next, void *ws, hipStream_t s);
+// Device scratch the log-softmax of R rows of V logits needs (ws above).
+size_t logsoftmax_ws_bytes(int R, int V);
 
 // CacheBlend selector: dev[p - p0] = ||K_fresh[p] - K_stale[p]|| + ||V_fresh[p] -
 // V_stale[p]|| over layer fl of `fresh` and layer sl of `stale` (cache

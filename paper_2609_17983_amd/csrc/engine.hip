@@ -56,6 +56,7 @@ struct kvr_ctx {
     size_t sel_bytes = 0;
     float *score_y = nullptr;     // hidden rows of the scored block [max rows][d]
     float *score_part = nullptr;  // logit tiles [split][64][vocab]
+    void *score_lsm = nullptr;    // log-softmax chunk statistics
     size_t score_bytes = 0;
 
     int rows_cap = 0;  // rows per pass
@@ -480,7 +481,7 @@ kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t 
         }
         const int nt = lp ? std::max(0, std::min(R, m - 1 - c0)) : 0;  // rows with a target to score
         KVR_SCHECK(launch_logsoftmax(c->score_part, nsplit, R, V, tokens + n + c0 + 1, nt, lp ? lp + c0 : nullptr,
-                                     argmax ? argmax + c0 : nullptr, (c0 + R == m) ? next : nullptr, s),
+                                     argmax ? argmax + c0 : nullptr, (c0 + R == m) ? next : nullptr, c->score_lsm, s),
                    "logsoftmax", ST_LOGSOFTMAX);
     }
 #undef KVR_SCHECK
@@ -492,13 +493,15 @@ kvr_status score_buffers(kvr_ctx *c) {
     const kvr_dims &d = c->d;
     const SkinnyPlan plan = plan_skinny(d.vocab / 16, d.d_model, false, 16, "KVR_NT_LM", "KVR_SPLIT_LM");
     const size_t y_bytes = align_up((size_t)c->rows_cap * d.d_model * 4, 256);
-    const size_t p_bytes = (size_t)std::max(plan.split, 1) * SCORE_ROWS * d.vocab * 4;
+    const size_t p_bytes = align_up((size_t)std::max(plan.split, 1) * SCORE_ROWS * d.vocab * 4, 256);
+    const size_t l_bytes = logsoftmax_ws_bytes(SCORE_ROWS, d.vocab);
     char *buf = nullptr;
-    hipError_t e = hipMalloc((void **)&buf, y_bytes + p_bytes);
+    hipError_t e = hipMalloc((void **)&buf, y_bytes + p_bytes + l_bytes);
     if (e != hipSuccess) return fail(c, KVR_E_NOMEM, "scoring buffer allocation failed");
     c->score_y = (float *)buf;
     c->score_part = (float *)(buf + y_bytes);
-    c->score_bytes = y_bytes + p_bytes;
+    c->score_lsm = buf + y_bytes + p_bytes;
+    c->score_bytes = y_bytes + p_bytes + l_bytes;
     return KVR_OK;
 }
 

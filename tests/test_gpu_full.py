@@ -151,6 +151,37 @@ def test_llama8b_attention_selector(llama):
     assert sure <= set(sel)
 
 
+def test_llama8b_score(llama):
+    """Fresh-query scoring at full size: 24 tokens appended after a 5000-position
+    synthetic cache, LM head tied to the 128256-entry embedding; teacher-forced
+    log-probabilities against the oracle, argmax where the top-two gap is clear."""
+    from oracle import scoring as osc
+    shape = llama.shape
+    m = 24
+    toks = synth.make_tokens(N + m, shape.vocab, seed=31)
+    cache = synth.make_stale_cache(shape, N + m, device="cuda", label=31)
+    ref_in = cache.to(torch.float64).cpu().numpy()
+    lp = torch.empty(m - 1, device="cuda")
+    am = torch.empty(m, dtype=torch.int32, device="cuda")
+    say(f"llama8b score n={N} m={m}")
+    kvr.kvr_score(llama.ctx, cache.data_ptr(), N, N + m, toks.cuda().data_ptr(), m, lp.data_ptr(), am.data_ptr(),
+                  torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    say("llama8b score: oracle")
+    ow = OracleWeights(llama.weights)
+    lm = llama.weights["embed"].to(torch.float64).cpu().numpy()
+    ref_lp, ref_am = osc.score(shape, ow, lm, ref_in.copy(), toks.numpy(), N, m)
+    err = relmax(lp.cpu().numpy(), ref_lp)
+    say(f"llama8b score: logprob err {err:.3e}")
+    assert err <= TOL[kvr.KVR_BF16]
+    y = od.repair(shape, ow, ref_in.copy(), toks.numpy(), N, N + m, [])
+    logits = y @ lm.T
+    top2 = np.sort(logits, axis=-1)[:, -2:]
+    clear = (top2[:, 1] - top2[:, 0]) > 2e-3 * np.max(np.abs(logits))
+    say(f"llama8b score: {int(clear.sum())} of {m} argmax decisions clear")
+    assert np.array_equal(am.cpu().numpy()[clear], ref_am[clear])
+
+
 def test_llama8b_batched_64_docs(llama):
     shape = llama.shape
     lens = synth.doc_lengths(64, 2000, 8000)

@@ -46,9 +46,13 @@ def _oracle_logits(shape, ow, lm, cache_np, toks, n, m):
     return y @ lm.T
 
 
-@pytest.mark.parametrize("dtype,n,m", [(kvr.KVR_F32, 480, 24), (kvr.KVR_BF16, 600, 40), (kvr.KVR_BF16, 500, 100)])
-def test_score_matches_oracle(dtype, n, m):
-    shape = synth.TINY if dtype == kvr.KVR_F32 else MID
+# vocabulary of 8208 = 16 * 513: five log-softmax chunks, the last one shorter
+MID_V = synth.ModelShape("mid-bf16-v8208", 2, 512, 8, 2, 128, 1024, 8208, 1e-5, 500000.0)
+
+
+@pytest.mark.parametrize("dtype,n,m,shape", [(kvr.KVR_F32, 480, 24, synth.TINY), (kvr.KVR_BF16, 600, 40, MID),
+                                             (kvr.KVR_BF16, 500, 100, MID), (kvr.KVR_BF16, 300, 33, MID_V)])
+def test_score_matches_oracle(dtype, n, m, shape):
     n_cap = n + m + 8
     eng, ow, lm, tdt = _setup(shape, dtype, n_cap, 128)
     try:
