@@ -236,8 +236,10 @@ bool pack_ok(const kvr_dims &d, bool force_simple) {
 
 bool skinny_pass_ok(const kvr_ctx *c, int R) { return c->wpk != nullptr && R <= 64; }
 
+// Packed weight: the tiled MFMA kernel, whose activations are in operand
+// order; otherwise the row-major simple kernel.
 hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
-    if (a.wp && a.ldx % 8 == 0) return launch_linear_tiled(epi, a, s);
+    if (a.wp) return launch_linear_tiled(epi, a, s);
     return launch_linear_simple(c->bf16, epi, a, s);
 }
 
@@ -315,6 +317,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     if (R == 0) return KVR_OK;
     const bool attn_mfma = c->bf16 && !c->force_simple && d.head_dim == ATT_HD && d.n_heads / d.n_kv_heads <= 16;
     const bool sk = skinny_pass_ok(c, R);
+    const bool op = c->wpk != nullptr;  // matrix operands in MFMA operand order (both packed-weight kernels)
     if (attn_mfma) plan_attention(c, t);
     if ((int)t.items.size() > c->items_cap || (int)t.comb.size() > c->comb_cap)
         return fail(c, KVR_E_RANGE, "attention plan exceeds the context's item capacity");
@@ -369,7 +372,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     for (int l = 0; l < n_run; ++l) {
         const kvr_layer_weights &w = c->layers[l];
         const kvr_ctx::PackedLayer pw = c->wpk ? c->pk[l] : kvr_ctx::PackedLayer{nullptr, nullptr, nullptr, nullptr};
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, op, s),
                   "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
@@ -388,14 +391,14 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
         if (attn_mfma) {
             KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, docs, items,
                                             (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
-                                            (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, lse, s),
+                                            (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, op, lse, s),
                       "attention", ST_ATTN);
             if (!t.comb.empty())
                 KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
-                                                   (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, sk, lse, s), "attention_combine", ST_COMBINE);
+                                                   (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, op, lse, s), "attention_combine", ST_COMBINE);
         } else {
             KVR_CHECK(launch_attention_simple(bf, c->Qb, c->Qb_lo, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob,
-                                              c->Ob_lo, sk, lse, s),
+                                              c->Ob_lo, op, lse, s),
                       "attention_simple", ST_ATTN);
         }
         if (mh) {
@@ -411,7 +414,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
         }
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, sk, s),
+        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, op, s),
                   "rmsnorm(mlp)", ST_NORM);
         resid_split = 0;
         if (sk) {
