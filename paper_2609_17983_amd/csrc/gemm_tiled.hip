@@ -7,6 +7,8 @@
 // with one 16-byte access per lane.  A block computes a 128 x 256 output tile
 // (8 row tiles x 16 weight tiles); its four wavefronts own 64 x 128 sub-tiles
 // (4 x 8 v_mfma_f32_16x16x32_bf16 tiles, two MFMAs per product for hi and lo).
+// When 128-row blocks would not give every compute unit two of them, the
+// launch takes 64 x 256 tiles (four wavefronts of 64 x 64), three per unit.
 //
 // The fragments go from memory straight into LDS (global_load_lds_dwordx4:
 // lane l's 16 bytes land at the destination + 16 l, so a fragment keeps its
@@ -36,18 +38,25 @@ namespace kvr {
 
 namespace {
 
-constexpr int RT = 8;           // 16-row activation tiles per block (128 rows)
 constexpr int WT = 16;          // 16-row weight tiles per block (256 output columns)
-constexpr int STAGES = 2;       // k-steps held in the LDS ring (two blocks per compute unit)
+constexpr int STAGES = 2;       // k-steps held in the LDS ring
 constexpr int FRAG = 512;       // bf16 elements of one 16 x 32 operand fragment
-constexpr int NFRAG = 2 * RT + WT;  // fragments per k-step: X hi, X lo, W
-constexpr int STAGE = NFRAG * FRAG;
-constexpr int FRAGS_PER_WAVE = NFRAG / 4;
 constexpr int XCDS = 8;         // L2 domains the workgroups are dealt to in turn
 constexpr int GROUP_M = 4;      // row blocks per group of the tile order
 
-static_assert(FRAGS_PER_WAVE == 8, "the wait counts below assume eight loads per wavefront per k-step");
-static_assert(STAGES >= 2 && STAGES <= 4, "wait counts cover at most two later k-steps in flight");
+// Block shape for RT 16-row activation tiles (8: 128 rows, two blocks per
+// compute unit; 4: 64 rows, three blocks per unit, for grids that would
+// otherwise not fill the chip): wavefronts in WM rows x WN columns, each
+// owning 4 row tiles x JT weight tiles.
+template <int RT>
+struct TileShape {
+    static constexpr int NFRAG = 2 * RT + WT;  // fragments per k-step: X hi, X lo, W
+    static constexpr int STAGE = NFRAG * FRAG;
+    static constexpr int FPW = NFRAG / 4;      // fragments each wavefront loads per k-step
+    static constexpr int WM = RT / 4, WN = 4 / WM, JT = WT / WN;
+    static constexpr int BLOCKS_PER_CU = RT == 8 ? 2 : 3;
+    static_assert(NFRAG % 4 == 0 && WM * WN == 4, "four wavefronts per block");
+};
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
 
@@ -59,21 +68,19 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_barrier" ::: "memory");
 }
 
-// Wait until at most n of this wavefront's vector-memory loads are in flight
-// (n in {0, 8, 16}; expcnt and lgkmcnt left unconstrained).
-template <int N>
-__device__ __forceinline__ void wait_loads() {
-    static_assert(N == 0 || N == 8 || N == 16, "unsupported wait count");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
-}
+// Wait until none of this wavefront's vector-memory loads is in flight
+// (expcnt and lgkmcnt left unconstrained).
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x70 | 0xF00); }
 
-template <int EPI>
-__global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
+template <int EPI, int RT>
+__global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tiled_kernel(LinearArgs a) {
+    using S = TileShape<RT>;
+    constexpr int STAGE = S::STAGE, FPW = S::FPW, JT = S::JT;
     __shared__ __attribute__((aligned(16))) bf16_t lds[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = w >> 1, wn = w & 1;
+    const int wm = w / S::WN, wn = w % S::WN;
     const int ksteps = a.K >> 5;
     const int ntiles = (a.N * (EPI == EPI_SWIGLU ? 2 : 1)) >> 4;
     const int rtiles = (a.R + 15) >> 4;
@@ -87,12 +94,15 @@ __global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
     const int ti = tile - grp * GROUP_M * NB;
     const int bn = ti / gm, bm = grp * GROUP_M + ti % gm;
 
-    // this wavefront's eight fragments of every k-step: f = 8w + i (X hi row
-    // tiles 0-7, X lo row tiles 0-7, then weight tiles 0-15)
-    const bf16_t *src[FRAGS_PER_WAVE];
+    // this wavefront's fragments of every k-step: f = FPW w + i (X hi row
+    // tiles, X lo row tiles, then weight tiles).  The array has a fixed size:
+    // a local array whose size depends on the template parameter, captured by
+    // the lambda below, made the host compiler drop the kernel's launch stub.
+    static_assert(FPW <= 8, "at most eight fragments per wavefront");
+    const bf16_t *src[8];
 #pragma unroll
-    for (int i = 0; i < FRAGS_PER_WAVE; ++i) {
-        const int f = FRAGS_PER_WAVE * w + i;
+    for (int i = 0; i < FPW; ++i) {
+        const int f = FPW * w + i;
         if (f < 2 * RT) {
             const int t = min(bm * RT + (f % RT), rtiles - 1);
             src[i] = (const bf16_t *)(f < RT ? a.x : a.x_lo) + ((size_t)t * ksteps * 64 + lane) * 8;
@@ -102,44 +112,39 @@ __global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
         }
     }
     auto issue = [&](int kk) {
-        bf16_t *st = lds + (kk % STAGES) * STAGE + FRAGS_PER_WAVE * w * FRAG;
+        bf16_t *st = lds + (kk % STAGES) * STAGE + FPW * w * FRAG;
 #pragma unroll
-        for (int i = 0; i < FRAGS_PER_WAVE; ++i)
+        for (int i = 0; i < FPW; ++i)
             __builtin_amdgcn_global_load_lds(src[i] + (size_t)kk * 512, st + i * FRAG, 16, 0, 0);
     };
 
-    f32x4 acc[4][8];
+    f32x4 acc[4][JT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < JT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < ksteps) issue(s);
     for (int kk = 0; kk < ksteps; ++kk) {
-        // this wavefront's loads of k-step kk are done once at most those of
-        // the later k-steps already issued (up to STAGES - 2) remain
-        const int later = min(STAGES - 2, ksteps - 1 - kk);
-        if (later >= 2) wait_loads<16>();
-        else if (later == 1) wait_loads<8>();
-        else wait_loads<0>();
+        wait_loads();   // this wavefront's loads of k-step kk (the only ones in flight)
         lds_barrier();  // every wavefront's loads of kk have landed; all reads of kk - 1 are done
         if (kk + STAGES - 1 < ksteps) issue(kk + STAGES - 1);  // into the slot k-step kk - 1 used
 
         const bf16_t *st = lds + (kk % STAGES) * STAGE + lane * 8;
-        bf16x8 av[4], al[4], bv[8];
+        bf16x8 av[4], al[4], bv[JT];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             av[i] = *reinterpret_cast<const bf16x8 *>(st + (wm * 4 + i) * FRAG);
             al[i] = *reinterpret_cast<const bf16x8 *>(st + (RT + wm * 4 + i) * FRAG);
         }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) bv[j] = *reinterpret_cast<const bf16x8 *>(st + (2 * RT + wn * 8 + j) * FRAG);
+        for (int j = 0; j < JT; ++j) bv[j] = *reinterpret_cast<const bf16x8 *>(st + (2 * RT + wn * JT + j) * FRAG);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < JT; ++j) {
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[i], bv[j], acc[i][j], 0, 0, 0);
             }
@@ -155,8 +160,8 @@ __global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
         bf16_t *Alo = (bf16_t *)a.out_lo;
         const bool gate_lane = (lane & 8) == 0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int t = bn * WT + wn * 8 + j;
+        for (int j = 0; j < JT; ++j) {
+            const int t = bn * WT + wn * JT + j;
             const int f = 8 * t + (lane & 7);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -172,8 +177,8 @@ __global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
     }
     float *out = (float *)a.out;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int t = bn * WT + wn * 8 + j;
+    for (int j = 0; j < JT; ++j) {
+        const int t = bn * WT + wn * JT + j;
         if (t >= ntiles) continue;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -190,16 +195,25 @@ __global__ __launch_bounds__(256, 2) void linear_tiled_kernel(LinearArgs a) {
 
 }  // namespace
 
+template <int RT>
+void launch_rt(int epi, const LinearArgs &a, int tiles, hipStream_t s) {
+    dim3 grid((tiles + XCDS - 1) / XCDS * XCDS);
+    if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE, RT>, grid, dim3(256), 0, s, a);
+    else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID, RT>, grid, dim3(256), 0, s, a);
+    else kvr_launch(linear_tiled_kernel<EPI_SWIGLU, RT>, grid, dim3(256), 0, s, a);
+}
+
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     if (a.R <= 0) return hipSuccess;
     if (!a.x_lo || !a.wp || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.K % 32 != 0 || vrows % 16 != 0) return hipErrorInvalidValue;
-    const int tiles = ((vrows / 16 + WT - 1) / WT) * (((a.R + 15) / 16 + RT - 1) / RT);
-    dim3 grid((tiles + XCDS - 1) / XCDS * XCDS);
-    if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE>, grid, dim3(256), 0, s, a);
-    else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID>, grid, dim3(256), 0, s, a);
-    else kvr_launch(linear_tiled_kernel<EPI_SWIGLU>, grid, dim3(256), 0, s, a);
+    const int rtiles = (a.R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
+    // 128-row blocks unless they would not give every compute unit its two
+    // blocks; then 64-row blocks, three per unit
+    const int tiles8 = (rtiles + 7) / 8 * nb;
+    if (tiles8 >= TileShape<8>::BLOCKS_PER_CU * 256) launch_rt<8>(epi, a, tiles8, s);
+    else launch_rt<4>(epi, a, (rtiles + 3) / 4 * nb, s);
     return hipGetLastError();
 }
 

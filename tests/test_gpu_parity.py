@@ -313,3 +313,32 @@ def test_mid_bias_gqa7_repair(mid_bias, K):
     shape, eng, ow, toks, new, stale_np = mid_bias
     A = osel.select_edit_local(333, 100, 116, K)
     _repair_case(shape, eng, ow, stale_np, new, 100, 116, A, f"mid-bias K={K}")
+
+
+# A wide feed-forward (8192 features: 1024 gate/up weight tiles) and 1100 rows
+# give the gate/up projection 9 x 64 = 576 blocks of 128 rows, enough for the
+# tiled kernel's 128-row shape (two blocks per compute unit); the other
+# projections of the same pass take the 64-row shape.  The last 128-row block
+# holds 5 of its 8 row tiles.
+WIDE = synth.ModelShape("wide-ffn-bf16", 1, 512, 8, 2, 128, 8192, 2048, 1e-5, 500000.0)
+
+
+def test_wide_prefill_both_tile_shapes():
+    shape, n = WIDE, 1100
+    w = synth.make_weights(shape, dtype=torch.bfloat16, seed=5)
+    eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=64)
+    try:
+        toks = synth.make_tokens(n, shape.vocab, seed=6)
+        cache = eng.new_cache(n)
+        hidden = torch.empty((n, shape.d_model), device="cuda")
+        say(f"case: {shape.name} prefill n={n}")
+        eng.prefill(toks.cuda(), cache, hidden)
+        torch.cuda.synchronize()
+        oc, oy = od.prefill(shape, OracleWeights(w), toks.numpy())
+        got = cache.to(torch.float64).cpu().numpy()
+        errs = {(l, kv): relmax(got[l, kv], oc[l, kv]) for l in range(shape.n_layers) for kv in range(2)}
+        errs["hidden"] = relmax(hidden.cpu().numpy(), oy)
+        say(f"  {errs}")
+        assert max(errs.values()) <= TOL[kvr.KVR_BF16]
+    finally:
+        eng.close()
