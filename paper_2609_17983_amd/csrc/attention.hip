@@ -14,8 +14,12 @@
 // accumulator into the B operand of O^T += V^T P^T (as a compensated pair, two
 // MFMAs per k-step): both operands enumerate the
 // 32 keys of a k-step in the same permuted order (slot j of lane group g <->
-// key 16*(j/4) + 4*g + j%4), so P never leaves registers; V is stored
-// transposed in LDS.  Softmax runs in the exp2 domain; the running max is only
+// key 16*(j/4) + 4*g + j%4), so P never leaves registers.  V is staged in LDS
+// in its own [key][dim] layout (16-byte stores) and the V^T operand is read
+// with gfx950's transposing LDS load (ds_read_b64_tr_b16: in each 16-lane
+// group, lane i receives element i%4 of the 8-byte chunks that lanes
+// 4m + i/4 address, m = 0..3), so each lane gets four keys of one dimension
+// per load.  Softmax runs in the exp2 domain; the running max is only
 // raised (and the accumulators rescaled) when a row's tile max exceeds it by
 // more than 2^8, which keeps every probability below 256.  The causal mask is
 // applied only on tiles that reach a row's own position.  The next K/V tile is
@@ -39,13 +43,19 @@ constexpr int HD = ATT_HD;
 constexpr int KT = ATT_KT;
 constexpr int WAVES = 8;           // wavefronts per block
 constexpr int NLD = 16 / WAVES;    // 16-byte K (and V) loads per thread per tile
-constexpr int KS_STRIDE = HD + 8;  // keys tile row stride (bf16)
-constexpr int VT_STRIDE = KT + 8;  // transposed values row stride (bf16)
+constexpr int KS_STRIDE = HD + 8;  // key and value tile row stride (bf16)
 constexpr int PART_ROW = HD + 4;   // floats per (head, row) partial: O[128], m, l
 constexpr float RESCALE_SLACK = 8.0f;  // log2 headroom before the running max is raised
 constexpr int COMBINE_NP = 16;         // partials per row loaded in one round by the combine
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS load (see above): four 16-bit values from the chunks that
+// the lane's 16-lane group addresses.
+__device__ __forceinline__ i16x4 lds_read_tr16(const bf16_t *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4 *)p);
+}
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 
 __device__ __forceinline__ bf16x8 ld16(const bf16_t *p) { return *reinterpret_cast<const bf16x8 *>(p); }
@@ -68,7 +78,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                                                                     int MT, float *part, bf16_t *O, bf16_t *O_lo,
                                                                     int o_perm, float *lse) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS_STRIDE];
-    __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * VT_STRIDE];
+    __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * KS_STRIDE];
 
     const AttnItem it = items[blockIdx.x];
     const DocInfo dc = docs[it.doc];
@@ -115,25 +125,19 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     u32x4 kreg[NLD], vreg[NLD];
 #define KVR_ATT_FETCH(kt_)                                                                                  \
     _Pragma("clang loop unroll(full)") for (int i = 0; i < NLD; ++i) {                                     \
-        /* K: key (tid + 64*WAVES*i)/16, dims (tid%16)*8; V: key tid%64, dims 8*(tid/64 + WAVES*i) */       \
+        /* K and V: key (tid + 64*WAVES*i)/16, dims (tid%16)*8 */                                           \
         const int ksrc = min((kt_) + ((tid + 64 * WAVES * i) >> 4), it.k1 - 1);                             \
         kreg[i] = *reinterpret_cast<const u32x4 *>(Kg + (size_t)ksrc * HD + (tid & 15) * 8);                \
-        const int vsrc = min((kt_) + (tid & 63), it.k1 - 1);                                                \
-        vreg[i] = *reinterpret_cast<const u32x4 *>(Vg + (size_t)vsrc * HD + 8 * ((tid >> 6) + WAVES * i));  \
+        vreg[i] = *reinterpret_cast<const u32x4 *>(Vg + (size_t)ksrc * HD + (tid & 15) * 8);                \
     }
     KVR_ATT_FETCH(it.k0)
     for (int kt = it.k0; kt < it.k1; kt += KT) {
         __syncthreads();
 #pragma clang loop unroll(full)
         for (int i = 0; i < NLD; ++i) {
-            *reinterpret_cast<u32x4 *>(&Ks[((tid + 64 * WAVES * i) >> 4) * KS_STRIDE + (tid & 15) * 8]) = kreg[i];
-            const int d0 = 8 * ((tid >> 6) + WAVES * i);
-            const unsigned int wv[4] = {vreg[i][0], vreg[i][1], vreg[i][2], vreg[i][3]};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Vt[(d0 + 2 * e) * VT_STRIDE + (tid & 63)] = (bf16_t)(wv[e] & 0xffffu);
-                Vt[(d0 + 2 * e + 1) * VT_STRIDE + (tid & 63)] = (bf16_t)(wv[e] >> 16);
-            }
+            const int row = ((tid + 64 * WAVES * i) >> 4) * KS_STRIDE + (tid & 15) * 8;
+            *reinterpret_cast<u32x4 *>(&Ks[row]) = kreg[i];
+            *reinterpret_cast<u32x4 *>(&Vs[row]) = vreg[i];
         }
         __syncthreads();
         if (kt + KT < it.k1) {
@@ -222,11 +226,13 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
             bf16x8 va[2];
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16_t *vr = &Vt[(nt * 16 + (lane & 15)) * VT_STRIDE + ks * 32 + 4 * g];
-                const uint2 lo = *reinterpret_cast<const uint2 *>(vr);
-                const uint2 hi = *reinterpret_cast<const uint2 *>(vr + 16);
-                const u32x4 u = {lo.x, lo.y, hi.x, hi.y};
-                va[ks] = __builtin_bit_cast(bf16x8, u);
+                // this lane addresses key ks*32 + 4g + m (then + 16), dims
+                // 16 nt + 4q .. +3, for m = (lane%16)/4, q = lane%4; it receives
+                // dim 16 nt + lane%16 of keys ks*32 + 4g + 0..3 and + 16 + 0..3
+                const bf16_t *vr = &Vs[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * KS_STRIDE + nt * 16 + 4 * (lane & 3)];
+                const i16x4 lo = lds_read_tr16(vr);
+                const i16x4 hi = lds_read_tr16(vr + 16 * KS_STRIDE);
+                va[ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
 #pragma unroll
             for (int i = 0; i < PPW; ++i) {
