@@ -114,6 +114,8 @@ struct LinearArgs {
                           // SWIGLU: operand type [R][ldo]
     void *out_lo;         // SWIGLU: low part of the compensated output, or null
     int32_t ldo;
+    int32_t split;        // tiled STORE only: K cut into `split` slices, partial
+                          // tiles out[s][R][ldo] summed by the consumer (<= 1: none)
 };
 
 // Skinny (R <= 64) linear layer: X in operand order, W packed in operand order
@@ -183,8 +185,12 @@ hipError_t launch_attention_combine(const CombineItem *items, int n_items, const
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
 // Skinny MFMA path (R <= 64); nt = 16-row weight tiles per block (1..8).
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s);
-// Tiled MFMA path for many rows (packed weight, K a multiple of 64).
+// Tiled MFMA path for many rows (packed weight, K a multiple of 32,
+// activations in operand order).
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
+// Output-tile blocks the tiled kernel launches for R rows and vrows weight
+// rows (before any K split), and how many of them the chip runs at once.
+int tiled_blocks(int R, int vrows, int *slots);
 // Repack up to three row-major bf16 matrices (rows [0,e0), [e0,e1), [e1,V) of
 // the virtual matrix; interleave: w0 = gate, w1 = up, tile t = gate rows
 // 8t..8t+7 then up rows 8t..8t+7) of K columns into operand order at dst.

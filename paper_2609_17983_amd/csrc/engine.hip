@@ -66,6 +66,7 @@ struct kvr_ctx {
     char *ws = nullptr;
     size_t ws_bytes = 0;
     float *H = nullptr, *P = nullptr;  // residual stream; projection outputs / split-K partials
+    size_t p_floats = 0;               // capacity of P
     // matrix operands; in bf16 each is a compensated pair (hi, lo)
     void *Xn = nullptr, *Qb = nullptr, *Ob = nullptr, *Ab = nullptr;
     void *Xn_lo = nullptr, *Qb_lo = nullptr, *Ob_lo = nullptr, *Ab_lo = nullptr;
@@ -252,6 +253,7 @@ LinearArgs make_args(const void *x, const void *x_lo, int ldx, int R, int K, int
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
     a.wp = wp;
     a.out = out; a.ldo = ldo;
+    a.split = 1;
     return a;
 }
 
@@ -263,6 +265,19 @@ hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N,
     a.ntiles = (epi == EPI_SWIGLU ? 2 * N : N) / 16;
     a.out = out; a.out_lo = out_lo; a.split = p.split;
     return launch_linear_skinny(epi, a, p.nt, s);
+}
+
+// K slices for a tiled projection of R rows into vrows outputs whose partial
+// tiles go to P: enough blocks for about two per compute unit, at least 16
+// k-steps per slice, and no more partial tiles than P holds (1: no split).
+int tiled_split(const kvr_ctx *c, int R, int vrows, int K) {
+    int slots = 0;
+    const int blocks = tiled_blocks(R, vrows, &slots);
+    if (blocks >= 2 * 256) return 1;
+    int split = (2 * 256 + blocks - 1) / blocks;
+    split = std::min(split, std::max(1, K / 32 / 16));
+    split = std::min<long long>(split, (long long)(c->p_floats / ((size_t)R * vrows)));
+    return std::max(1, std::min(split, SPLIT_MAX));
 }
 
 // Step profiler: arm() hands two events to the next kernel launch, which
@@ -380,9 +395,11 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                       ST_QKV);
             qkv_split = p_qkv.split;
         } else {
-            KVR_CHECK(linear(c, EPI_STORE, make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P,
-                                                 nullptr, NQKV), s),
-                      "qkv", ST_QKV);
+            LinearArgs a = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr,
+                                     NQKV);
+            if (pw.qkv) a.split = tiled_split(c, R, NQKV, D);
+            KVR_CHECK(linear(c, EPI_STORE, a, s), "qkv", ST_QKV);
+            qkv_split = a.split;
         }
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
                                       hd, c->rope_cos, c->rope_sin, c->Qb, c->Qb_lo, s), "rope_scatter", ST_ROPE);
@@ -410,6 +427,12 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
         if (sk) {
             KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
             resid_split = p_o.split;
+        } else if (pw.o) {
+            // packed: partial tiles into P (the next RMSNorm adds them to H)
+            LinearArgs a = make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->P, nullptr, D);
+            a.split = tiled_split(c, R, D, qd);
+            KVR_CHECK(linear(c, EPI_STORE, a, s), "o_proj", ST_OPROJ);
+            resid_split = a.split;
         } else {
             KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
@@ -427,9 +450,17 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu,
                                                   c->Ab, c->Ab_lo, F), s),
                       "gate_up", ST_GATEUP);
-            KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down,
-                                                 c->H, nullptr, D), s),
-                      "down", ST_DOWN);
+            if (pw.down) {
+                LinearArgs a = make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down, c->P,
+                                         nullptr, D);
+                a.split = tiled_split(c, R, D, F);
+                KVR_CHECK(linear(c, EPI_STORE, a, s), "down", ST_DOWN);
+                resid_split = a.split;
+            } else {
+                KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D,
+                                                         pw.down, c->H, nullptr, D), s),
+                          "down", ST_DOWN);
+            }
         }
     }
     KVR_CHECK(launch_final_norm(bf, c->H, c->P, resid_split, c->final_norm, rows, docs, R, D, d.rms_eps, s),
@@ -604,6 +635,7 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     if (e != hipSuccess) { delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: workspace allocation failed"); }
     c->H = (float *)(c->ws + o_H);
     c->P = (float *)(c->ws + o_P);
+    c->p_floats = p_floats;
     c->Xn = c->ws + o_Xn;
     c->Qb = c->ws + o_Qb;
     c->Ob = c->ws + o_Ob;

@@ -9,6 +9,9 @@
 // (4 x 8 v_mfma_f32_16x16x32_bf16 tiles, two MFMAs per product for hi and lo).
 // When 128-row blocks would not give every compute unit two of them, the
 // launch takes 64 x 256 tiles (four wavefronts of 64 x 64), three per unit.
+// A STORE launch may also cut K into `split` slices (grid dimension y), each
+// writing an fp32 partial tile that the consumer sums in a fixed order: the
+// way a few hundred rows still fill the chip.
 //
 // The fragments go from memory straight into LDS (global_load_lds_dwordx4:
 // lane l's 16 bytes land at the destination + 16 l, so a fragment keeps its
@@ -32,6 +35,8 @@
 // XCD x runs range x in order: the blocks an XCD runs together cover about
 // four row blocks by eight column blocks, whose activation and weight slabs
 // its L2 shares.
+#include <algorithm>
+
 #include "common.h"
 
 namespace kvr {
@@ -81,7 +86,11 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w / S::WN, wn = w % S::WN;
-    const int ksteps = a.K >> 5;
+    const int ksteps = a.K >> 5;   // k-steps of the whole row (operand strides)
+    const int split = EPI == EPI_STORE ? max(1, a.split) : 1;
+    const int sp = blockIdx.y;    // this block's K slice: k-steps [k0, k0 + nk)
+    const int k0 = (int)(((long long)ksteps * sp) / split);
+    const int nk = (int)(((long long)ksteps * (sp + 1)) / split) - k0;
     const int ntiles = (a.N * (EPI == EPI_SWIGLU ? 2 : 1)) >> 4;
     const int rtiles = (a.R + 15) >> 4;
     // this workgroup's output tile (bm, bn) in the XCD-grouped order
@@ -115,7 +124,7 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
         bf16_t *st = lds + (kk % STAGES) * STAGE + FPW * w * FRAG;
 #pragma unroll
         for (int i = 0; i < FPW; ++i)
-            __builtin_amdgcn_global_load_lds(src[i] + (size_t)kk * 512, st + i * FRAG, 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(src[i] + (size_t)(k0 + kk) * 512, st + i * FRAG, 16, 0, 0);
     };
 
     f32x4 acc[4][JT];
@@ -126,11 +135,11 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
 
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
-        if (s < ksteps) issue(s);
-    for (int kk = 0; kk < ksteps; ++kk) {
+        if (s < nk) issue(s);
+    for (int kk = 0; kk < nk; ++kk) {
         wait_loads();   // this wavefront's loads of k-step kk (the only ones in flight)
         lds_barrier();  // every wavefront's loads of kk have landed; all reads of kk - 1 are done
-        if (kk + STAGES - 1 < ksteps) issue(kk + STAGES - 1);  // into the slot k-step kk - 1 used
+        if (kk + STAGES - 1 < nk) issue(kk + STAGES - 1);  // into the slot k-step kk - 1 used
 
         const bf16_t *st = lds + (kk % STAGES) * STAGE + lane * 8;
         bf16x8 av[4], al[4], bv[JT];
@@ -175,7 +184,7 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
         }
         return;
     }
-    float *out = (float *)a.out;
+    float *out = (float *)a.out + (size_t)sp * a.R * a.ldo;
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
         const int t = bn * WT + wn * JT + j;
@@ -197,10 +206,21 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
 
 template <int RT>
 void launch_rt(int epi, const LinearArgs &a, int tiles, hipStream_t s) {
-    dim3 grid((tiles + XCDS - 1) / XCDS * XCDS);
+    dim3 grid((tiles + XCDS - 1) / XCDS * XCDS, epi == EPI_STORE ? std::max(1, (int)a.split) : 1);
     if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE, RT>, grid, dim3(256), 0, s, a);
     else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID, RT>, grid, dim3(256), 0, s, a);
     else kvr_launch(linear_tiled_kernel<EPI_SWIGLU, RT>, grid, dim3(256), 0, s, a);
+}
+
+int tiled_blocks(int R, int vrows, int *slots) {
+    const int rtiles = (R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
+    const int tiles8 = (rtiles + 7) / 8 * nb;
+    if (tiles8 >= TileShape<8>::BLOCKS_PER_CU * 256) {
+        if (slots) *slots = TileShape<8>::BLOCKS_PER_CU * 256;
+        return tiles8;
+    }
+    if (slots) *slots = TileShape<4>::BLOCKS_PER_CU * 256;
+    return (rtiles + 3) / 4 * nb;
 }
 
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
@@ -208,6 +228,7 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     if (!a.x_lo || !a.wp || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.K % 32 != 0 || vrows % 16 != 0) return hipErrorInvalidValue;
+    if (a.split > 1 && (epi != EPI_STORE || a.split > a.K / 32)) return hipErrorInvalidValue;
     const int rtiles = (a.R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
     // 128-row blocks unless they would not give every compute unit its two
     // blocks; then 64-row blocks, three per unit
