@@ -204,24 +204,41 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
 }
 
 // Weight tiles per block and split-K factor of a skinny projection.  The X
-// operand is re-read from L2 once per block column, so blocks are made as wide
-// as the grid allows: split (a power of two, never for SwiGLU) doubles while a
-// wavefront's K slice stays above `wave_ks` k-steps and keeps at least 8, and
-// NT = ceil(ntiles * split / 256) tiles (at most 8) gives about one block per
-// compute unit.  wave_ks is 16 for the QKV projection and the LM head and 8
-// for the output and down projections (measured on the 8B shape: O 12.8 us at
-// split 4 against 13.9 at split 2; QKV 17.0 at split 2 against 17.7 at 4).
+// operand is re-read from L2 once per block column, so blocks are wide; a
+// block streams NT tiles over its K slice, and blocks beyond one per compute
+// unit run in a further round.  The plan minimises
+//   rounds * NT * k-steps per slice,   rounds = ceil(blocks / 256),
+// over NT <= 8 (7 for 64 rows, whose accumulators would spill at 8) and
+// splits up to the largest power of two that keeps each wavefront's K slice
+// above `wave_ks` k-steps (and at least 8), never splitting SwiGLU; ties go to
+// the wider block, then the smaller split.  wave_ks is 16 for the QKV
+// projection and the LM head and 8 for the output and down projections.
+// Measured on the 8B shape this reproduces the best of the swept plans
+// (QKV 3 x 2, O 4 x 4, gate/up 7, down 8 x 8); on the Qwen2.5-7B shape it
+// takes gate/up 5 (474 blocks; 67 us against 77-85 us at 8) and down 7 x 8
+// (32 us against 43 us at 8 x 16).
 struct SkinnyPlan { int nt, split; };
 
-SkinnyPlan plan_skinny(int ntiles, int K, bool swiglu, int wave_ks, const char *env_nt, const char *env_split) {
+SkinnyPlan plan_skinny(int ntiles, int K, int R, bool swiglu, int wave_ks, const char *env_nt,
+                       const char *env_split) {
     const int ksteps = K / 32;
-    SkinnyPlan p{1, 1};
+    int smax = 1;
     if (!swiglu)
-        while (p.split * 2 <= SPLIT_MAX && ksteps / (4 * p.split) > wave_ks && ksteps / (8 * p.split) >= 8)
-            p.split *= 2;
+        while (smax * 2 <= SPLIT_MAX && ksteps / (4 * smax) > wave_ks && ksteps / (8 * smax) >= 8) smax *= 2;
+    const int ntmax = (R + 15) / 16 >= 4 ? 7 : 8;
+    SkinnyPlan p{1, 1};
+    long long best = -1;
+    for (int sp = 1; sp <= smax; sp *= 2)
+        for (int nt = 1; nt <= ntmax; ++nt) {
+            const long long blocks = (long long)((ntiles + nt - 1) / nt) * sp;
+            const long long cost = (blocks + 255) / 256 * nt * ((ksteps + sp - 1) / sp);
+            if (best < 0 || cost < best || (cost == best && nt > p.nt)) {
+                p = SkinnyPlan{nt, sp};
+                best = cost;
+            }
+        }
     const int es = env_split ? env_int(env_split, 0) : 0;
     if (!swiglu && es >= 1) p.split = std::min(es, std::min(SPLIT_MAX, ksteps));
-    p.nt = std::max(1, std::min(8, (ntiles * p.split + 255) / 256));
     const int nt = env_int(env_nt, 0);
     if (nt >= 1 && nt <= 8) p.nt = nt;
     return p;
@@ -367,10 +384,10 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     const bool bf = c->bf16;
     SkinnyPlan p_qkv{}, p_o{}, p_gu{}, p_down{};
     if (sk) {
-        p_qkv = plan_skinny(NQKV / 16, D, false, 16, "KVR_NT_QKV", "KVR_SPLIT_QKV");
-        p_o = plan_skinny(D / 16, qd, false, 8, "KVR_NT_O", "KVR_SPLIT_O");
-        p_gu = plan_skinny(2 * F / 16, D, true, 16, "KVR_NT_GATEUP", nullptr);
-        p_down = plan_skinny(D / 16, F, false, 8, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
+        p_qkv = plan_skinny(NQKV / 16, D, R, false, 16, "KVR_NT_QKV", "KVR_SPLIT_QKV");
+        p_o = plan_skinny(D / 16, qd, R, false, 8, "KVR_NT_O", "KVR_SPLIT_O");
+        p_gu = plan_skinny(2 * F / 16, D, R, true, 16, "KVR_NT_GATEUP", nullptr);
+        p_down = plan_skinny(D / 16, F, R, false, 8, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
     }
 #define KVR_CHECK(expr, what, step)                                                \
     do {                                                                           \
@@ -483,7 +500,7 @@ kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t 
     for (int j = 0; j < m; ++j) t.rows.push_back(RowInfo{n + j, 0, j, 0});
     kvr_status st = run_pass(c, t, s);
     if (st != KVR_OK) return st;
-    const SkinnyPlan plan = plan_skinny(V / 16, D, false, 16, "KVR_NT_LM", "KVR_SPLIT_LM");
+    const SkinnyPlan plan = plan_skinny(V / 16, D, SCORE_ROWS, false, 16, "KVR_NT_LM", "KVR_SPLIT_LM");
 #define KVR_SCHECK(expr, what, step)                                                \
     do {                                                                           \
         hipError_t err_ = arm(c);                                                  \
@@ -525,7 +542,7 @@ kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t 
 kvr_status score_buffers(kvr_ctx *c) {
     if (c->score_y) return KVR_OK;
     const kvr_dims &d = c->d;
-    const SkinnyPlan plan = plan_skinny(d.vocab / 16, d.d_model, false, 16, "KVR_NT_LM", "KVR_SPLIT_LM");
+    const SkinnyPlan plan = plan_skinny(d.vocab / 16, d.d_model, SCORE_ROWS, false, 16, "KVR_NT_LM", "KVR_SPLIT_LM");
     const size_t y_bytes = align_up((size_t)c->rows_cap * d.d_model * 4, 256);
     const size_t p_bytes = align_up((size_t)std::max(plan.split, 1) * SCORE_ROWS * d.vocab * 4, 256);
     const size_t l_bytes = logsoftmax_ws_bytes(SCORE_ROWS, d.vocab);
