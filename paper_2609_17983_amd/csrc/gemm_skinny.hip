@@ -190,9 +190,6 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
         case 6: return launch_nt<6>(epi, a, s);
         case 7: return launch_nt<7>(epi, a, s);
         case 8: return launch_nt<8>(epi, a, s);
-        case 12: return launch_nt<12>(epi, a, s);
-        case 14: return launch_nt<14>(epi, a, s);
-        case 16: return launch_nt<16>(epi, a, s);
         default: return hipErrorInvalidValue;
     }
 }
