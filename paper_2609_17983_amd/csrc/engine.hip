@@ -148,7 +148,11 @@ struct Tables {
 
 // Split the key ranges of the row blocks over work items: without splitting
 // when there are enough items to fill the GPU, otherwise in chunks of KS keys
-// (multiple of the 64-key tile) so that about `target` items exist.
+// (a multiple of the 64-key tile, at least two tiles) so that about `target`
+// items exist.  The attention kernel runs one block per compute unit, so the
+// target is one item per unit: more, shorter items cost a second round and a
+// longer combine (Mistral shape, 48 rows at 4900-4950: 0.92 ms of attention
+// and combine per repair at 768 items against 0.64 ms at 256).
 void plan_attention(const kvr_ctx *c, Tables &t) {
     const int Hkv = c->d.n_kv_heads;
     const int G = c->d.n_heads / Hkv;
@@ -162,7 +166,7 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
             blocks.push_back({di, dc.row0 + b, nb, t.rows[dc.row0 + b + nb - 1].pos + 1});
         }
     }
-    const int target = env_int("KVR_ATT_TARGET", 768);
+    const int target = env_int("KVR_ATT_TARGET", 256);
     long long total_keys = 0;
     for (auto &b : blocks) total_keys += b.kmax;
     int KS = 1 << 30;

@@ -342,3 +342,21 @@ def test_wide_prefill_both_tile_shapes():
         assert max(errs.values()) <= TOL[kvr.KVR_BF16]
     finally:
         eng.close()
+
+
+def test_wide_repair_split_tiled_projections():
+    """166 repaired rows (above the skinny kernel's 64) of the wide shape: the
+    tiled projections with K split into slices (down over 8192 features,
+    output over 1024), their partial tiles summed by the next row kernel."""
+    shape, n = WIDE, 900
+    w = synth.make_weights(shape, dtype=torch.bfloat16, seed=7)
+    eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=256)
+    try:
+        ow = OracleWeights(w, cache=True)
+        stale = synth.make_stale_cache(shape, n, label=7).to(torch.float64).numpy()
+        toks = synth.make_tokens(n, shape.vocab, seed=8)
+        new = synth.apply_edit(toks, 200, 16, shape.vocab)
+        A = osel.select_edit_local(n, 200, 216, 150)
+        _repair_case(shape, eng, ow, stale, new, 200, 216, A, f"{shape.name} EditLocal K=150 (166 rows)")
+    finally:
+        eng.close()
