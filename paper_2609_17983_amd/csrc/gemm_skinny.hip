@@ -45,7 +45,7 @@ template <int MT, int NT, int EPI>
 __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     constexpr int FW = 16 * NT;          // virtual weight rows of a block
     constexpr int D = NT >= 6 ? 2 : 3;   // k-steps in flight per wavefront
-    __shared__ float red[MT * 16][FW];
+    __shared__ float red[4][MT * 16][FW];  // each wavefront's partial sums
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int split = a.split;
@@ -113,22 +113,17 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
             if (s + j < s1) mma(j);
     }
 
-    // sum the four wavefronts in a fixed order; accumulator layout: lane l holds
-    // column l%16, rows 4*(l/16)+e
-    for (int q = 0; q < 4; ++q) {
-        if (w == q) {
+    // every wavefront stores its partial sums (accumulator layout: lane l holds
+    // column l%16, rows 4*(l/16)+e); after one barrier each output is the sum
+    // over the four wavefronts in a fixed order
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
+        for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float &d = red[mt * 16 + 4 * (lane >> 4) + e][nt * 16 + (lane & 15)];
-                        d = (q == 0 ? 0.f : d) + acc[mt][nt][e];
-                    }
-        }
-        __syncthreads();
-    }
+            for (int e = 0; e < 4; ++e) red[w][mt * 16 + 4 * (lane >> 4) + e][nt * 16 + (lane & 15)] = acc[mt][nt][e];
+    __syncthreads();
+    auto total = [&](int r, int c) { return ((red[0][r][c] + red[1][r][c]) + red[2][r][c]) + red[3][r][c]; };
 
     const int R = a.R;
     const int tiles_here = min(NT, a.ntiles - tg * NT);
@@ -140,7 +135,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         for (int i = threadIdx.x; i < R * nf; i += 256) {
             const int r = i / nf, c = i - r * nf;
             const int nt = c >> 3, j = c & 7;
-            const float g = red[r][16 * nt + j], u = red[r][16 * nt + 8 + j];
+            const float g = total(r, 16 * nt + j), u = total(r, 16 * nt + 8 + j);
             store_operand(A, Al, perm_offset(r, 8 * (tg * NT + nt) + j, a.N), silu_f(g) * u);
         }
     } else {
@@ -148,7 +143,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         const int nc = 16 * tiles_here;
         for (int i = threadIdx.x; i < R * nc; i += 256) {
             const int r = i / nc, c = i - r * nc;
-            out[(size_t)r * a.N + tg * FW + c] = red[r][c];
+            out[(size_t)r * a.N + tg * FW + c] = total(r, c);
         }
     }
 }
