@@ -73,7 +73,7 @@ __device__ __forceinline__ float xsum4(float v) {
 // PPW: (head, row tile) pairs per wavefront; MT: row tiles of a full item.
 template <int PPW>
 __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t *Q, const bf16_t *Q_lo,
-                                                                    const RowInfo *rows, const DocInfo *docs,
+                                                                    const RowInfo *rows,
                                                                     const AttnItem *items, int layer, int Hq, int Hkv,
                                                                     int MT, float *part, bf16_t *O, bf16_t *O_lo,
                                                                     int o_perm, float *lse) {
@@ -81,16 +81,15 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * KS_STRIDE];
 
     const AttnItem it = items[blockIdx.x];
-    const DocInfo dc = docs[it.doc];
     const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront index (uniform)
     const int G = Hq / Hkv;
     const int qd = Hq * HD;
     const int MTi = (it.nrows + 15) >> 4;  // row tiles this item has
     const int npairs = G * MTi;
-    const size_t head_stride = (size_t)dc.n_cap * HD;
-    const bf16_t *Kg = (const bf16_t *)dc.cache + (((size_t)layer * 2 + 0) * Hkv + it.kvh) * head_stride;
-    const bf16_t *Vg = (const bf16_t *)dc.cache + (((size_t)layer * 2 + 1) * Hkv + it.kvh) * head_stride;
+    const size_t head_stride = (size_t)it.n_cap * HD;
+    const bf16_t *Kg = (const bf16_t *)it.cache + (((size_t)layer * 2 + 0) * Hkv + it.kvh) * head_stride;
+    const bf16_t *Vg = (const bf16_t *)it.cache + (((size_t)layer * 2 + 1) * Hkv + it.kvh) * head_stride;
 
     // this wavefront's pairs: p = w + WAVES*i -> head t = p / MTi, row tile p % MTi
     bool pvalid[PPW];
@@ -341,7 +340,7 @@ int attention_row_tiles(int Hq, int Hkv) {
     return G >= 16 ? 1 : std::min(4, std::max(1, 16 / G));
 }
 
-hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
+hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O,
                                  bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
@@ -349,10 +348,10 @@ hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowI
     const int MT = attention_row_tiles(Hq, Hkv);
     const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
     if (ppw == 1)
-        kvr_launch(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+        kvr_launch(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items,
                            layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
     else if (ppw == 2)
-        kvr_launch(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, docs, items,
+        kvr_launch(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items,
                            layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
     else
         return hipErrorInvalidValue;

@@ -86,7 +86,8 @@ struct AttnItem {
     int32_t kvh;
     int32_t k0, k1;
     int32_t part;
-    int32_t pad;
+    int32_t n_cap;        // the document's cache (copied from its DocInfo so
+    const void *cache;    // that the key/value loads need no second lookup)
 };
 
 // Combine step for rows whose keys were split over several items.
@@ -177,7 +178,7 @@ hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, c
 // 16-row tiles per attention work item for a head grouping (items carry up to
 // 16 * this many rows).
 int attention_row_tiles(int Hq, int Hkv);
-hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows, const DocInfo *docs,
+hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows,
                                  const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
                                  float *part, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s);
 hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,

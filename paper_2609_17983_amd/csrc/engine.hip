@@ -191,14 +191,15 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
         const int ns = (b.kmax + KS - 1) / KS;
         for (int g = 0; g < Hkv; ++g) {
             if (ns <= 1) {
-                t.items.push_back({b.doc, b.row0, b.nrows, g, 0, b.kmax, -1, 0});
+                t.items.push_back({b.doc, b.row0, b.nrows, g, 0, b.kmax, -1, t.docs[b.doc].n_cap, t.docs[b.doc].cache});
                 continue;
             }
             CombineItem ci{};
             ci.row0 = b.row0; ci.nrows = b.nrows; ci.kvh = g; ci.part0 = next_slot; ci.nparts = ns;
             t.comb.push_back(ci);
             for (int s = 0; s < ns; ++s)
-                t.items.push_back({b.doc, b.row0, b.nrows, g, s * KS, std::min(b.kmax, (s + 1) * KS), next_slot + s, 0});
+                t.items.push_back({b.doc, b.row0, b.nrows, g, s * KS, std::min(b.kmax, (s + 1) * KS), next_slot + s,
+                                   t.docs[b.doc].n_cap, t.docs[b.doc].cache});
             next_slot += ns;
         }
     }
@@ -427,7 +428,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
         if (l == kv_layer) return KVR_OK;
         float *lse = mh ? mh->lse : nullptr;
         if (attn_mfma) {
-            KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, docs, items,
+            KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, items,
                                             (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
                                             (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, op, lse, s),
                       "attention", ST_ATTN);
