@@ -45,7 +45,7 @@ template <int MT, int NT, int EPI>
 __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     constexpr int FW = 16 * NT;          // virtual weight rows of a block
     constexpr int D = NT >= 6 ? 2 : 3;   // k-steps in flight per wavefront
-    __shared__ float red[4][MT * 16][FW];  // each wavefront's partial sums
+    __shared__ __attribute__((aligned(16))) float red[4][MT * 16 * (FW + 4)];  // each wavefront's partial sums
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int split = a.split;
@@ -116,34 +116,59 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     // every wavefront stores its partial sums (accumulator layout: lane l holds
     // column l%16, rows 4*(l/16)+e); after one barrier each output is the sum
     // over the four wavefronts in a fixed order
+    constexpr int LD = FW + 4;  // padded row: the four row groups of a store fall on different banks
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) red[w][mt * 16 + 4 * (lane >> 4) + e][nt * 16 + (lane & 15)] = acc[mt][nt][e];
+            for (int e = 0; e < 4; ++e) red[w][(mt * 16 + 4 * (lane >> 4) + e) * LD + nt * 16 + (lane & 15)] = acc[mt][nt][e];
     __syncthreads();
-    auto total = [&](int r, int c) { return ((red[0][r][c] + red[1][r][c]) + red[2][r][c]) + red[3][r][c]; };
+    auto total4 = [&](int r, int c) {
+        const int i = r * LD + c;
+        const f32x4 v0 = *reinterpret_cast<const f32x4 *>(&red[0][i]), v1 = *reinterpret_cast<const f32x4 *>(&red[1][i]);
+        const f32x4 v2 = *reinterpret_cast<const f32x4 *>(&red[2][i]), v3 = *reinterpret_cast<const f32x4 *>(&red[3][i]);
+        return ((v0 + v1) + v2) + v3;
+    };
 
     const int R = a.R;
     const int tiles_here = min(NT, a.ntiles - tg * NT);
     if (EPI == EPI_SWIGLU) {
-        // tile nt, column j < 8: gate of feature 8*(tg*NT+nt)+j; column j+8: its up
+        // item (r, nt): the 8 features of weight tile nt for row r (gate in
+        // columns 0-7 of the tile, up in 8-15) are 16 contiguous bytes of the
+        // operand-order output, hi and lo
         bf16_t *A = (bf16_t *)a.out;
         bf16_t *Al = (bf16_t *)a.out_lo;
-        const int nf = 8 * tiles_here;
-        for (int i = threadIdx.x; i < R * nf; i += 256) {
-            const int r = i / nf, c = i - r * nf;
-            const int nt = c >> 3, j = c & 7;
-            const float g = total(r, 16 * nt + j), u = total(r, 16 * nt + 8 + j);
-            store_operand(A, Al, perm_offset(r, 8 * (tg * NT + nt) + j, a.N), silu_f(g) * u);
+        for (int i = threadIdx.x; i < MT * 16 * NT; i += 256) {
+            const int r = i / NT, nt = i - r * NT;
+            if (r >= R || nt >= tiles_here) continue;
+            const f32x4 g0 = total4(r, 16 * nt), g1 = total4(r, 16 * nt + 4);
+            const f32x4 u0 = total4(r, 16 * nt + 8), u1 = total4(r, 16 * nt + 12);
+            float y[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                y[e] = silu_f(g0[e]) * u0[e];
+                y[4 + e] = silu_f(g1[e]) * u1[e];
+            }
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bf16_t h0 = f32_to_bf16(y[2 * e]), h1 = f32_to_bf16(y[2 * e + 1]);
+                const bf16_t l0 = f32_to_bf16(y[2 * e] - bf16_to_f32(h0)), l1 = f32_to_bf16(y[2 * e + 1] - bf16_to_f32(h1));
+                hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                lo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+            }
+            const size_t off = perm_offset(r, 8 * (tg * NT + nt), a.N);
+            *reinterpret_cast<u32x4 *>(A + off) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+            *reinterpret_cast<u32x4 *>(Al + off) = u32x4{lo[0], lo[1], lo[2], lo[3]};
         }
     } else {
-        float *out = (float *)a.out + (size_t)sp * R * a.N;
-        const int nc = 16 * tiles_here;
-        for (int i = threadIdx.x; i < R * nc; i += 256) {
-            const int r = i / nc, c = i - r * nc;
-            out[(size_t)r * a.N + tg * FW + c] = total(r, c);
+        float *out = (float *)a.out + (size_t)sp * R * a.N + tg * FW;
+        constexpr int C4 = FW / 4;
+        for (int i = threadIdx.x; i < MT * 16 * C4; i += 256) {
+            const int r = i / C4, c = 4 * (i - r * C4);
+            if (r >= R || c >= 16 * tiles_here) continue;
+            *reinterpret_cast<f32x4 *>(out + (size_t)r * a.N + c) = total4(r, c);
         }
     }
 }
@@ -175,6 +200,9 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.R > 64 || a.K % 32 != 0 || a.split < 1 || (epi == EPI_SWIGLU && a.split != 1) || vrows % 16 != 0 ||
         a.ntiles != vrows / 16)
+        return hipErrorInvalidValue;
+    // the epilogue stores 16 bytes at a time
+    if (((uintptr_t)a.out & 15) != 0 || ((uintptr_t)a.out_lo & 15) != 0 || (epi == EPI_SWIGLU && a.N % 32 != 0))
         return hipErrorInvalidValue;
     switch (nt) {
         case 1: return launch_nt<1>(epi, a, s);
