@@ -71,14 +71,16 @@ __device__ __forceinline__ float xsum4(float v) {
 }
 
 // PPW: (head, row tile) pairs per wavefront; MT: row tiles of a full item.
-template <int PPW>
+template <int PPW, int KG>
 __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t *Q, const bf16_t *Q_lo,
                                                                     const RowInfo *rows,
                                                                     const AttnItem *items, int layer, int Hq, int Hkv,
                                                                     int MT, float *part, bf16_t *O, bf16_t *O_lo,
                                                                     int o_perm, float *lse) {
-    __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS_STRIDE];
-    __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * KS_STRIDE];
+    // KG 64-key K tiles, then KG V tiles (one per key group); after the key
+    // loop the same memory takes the second key group's softmax state
+    __shared__ __attribute__((aligned(16))) bf16_t kv_lds[2 * KG * KT * KS_STRIDE];
+    bf16_t *Ks = kv_lds, *Vs = kv_lds + KG * KT * KS_STRIDE;
 
     const AttnItem it = items[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4;
@@ -87,6 +89,12 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     const int qd = Hq * HD;
     const int MTi = (it.nrows + 15) >> 4;  // row tiles this item has
     const int npairs = G * MTi;
+    // KG = 2: the wavefronts form two key groups that take alternate 64-key
+    // tiles (each pair is worked by two wavefronts, one per group) and merge
+    // their softmax states at the end (items of at most four pairs).
+    static_assert(KG == 1 || KG == 2, "key groups");
+    constexpr int WG = WAVES / KG;
+    const int kg = w / WG, lw = w - kg * WG;
     const size_t head_stride = (size_t)it.n_cap * HD;
     const bf16_t *Kg = (const bf16_t *)it.cache + (((size_t)layer * 2 + 0) * Hkv + it.kvh) * head_stride;
     const bf16_t *Vg = (const bf16_t *)it.cache + (((size_t)layer * 2 + 1) * Hkv + it.kvh) * head_stride;
@@ -99,7 +107,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     float m[PPW], l[PPW];
 #pragma unroll
     for (int i = 0; i < PPW; ++i) {
-        const int p = w + WAVES * i;
+        const int p = lw + WG * i;
         pvalid[i] = p < npairs;
         pt[i] = pvalid[i] ? p / MTi : 0;
         pm[i] = pvalid[i] ? p % MTi : 0;
@@ -120,28 +128,36 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     const float sc = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
     const int minpos = rows[it.row0].pos;  // rows ascend: every row sees all keys <= minpos
 
-    // the next key tile is fetched into registers while the current one is used
-    u32x4 kreg[NLD], vreg[NLD];
-#define KVR_ATT_FETCH(kt_)                                                                                  \
-    _Pragma("clang loop unroll(full)") for (int i = 0; i < NLD; ++i) {                                     \
-        /* K and V: key (tid + 64*WAVES*i)/16, dims (tid%16)*8 */                                           \
-        const int ksrc = min((kt_) + ((tid + 64 * WAVES * i) >> 4), it.k1 - 1);                             \
-        kreg[i] = *reinterpret_cast<const u32x4 *>(Kg + (size_t)ksrc * HD + (tid & 15) * 8);                \
-        vreg[i] = *reinterpret_cast<const u32x4 *>(Vg + (size_t)ksrc * HD + (tid & 15) * 8);                \
+    // the next KG key tiles are fetched into registers while the current ones are used
+    u32x4 kreg[KG][NLD], vreg[KG][NLD];
+#define KVR_ATT_FETCH(kb_)                                                                                  \
+    _Pragma("clang loop unroll(full)") for (int q = 0; q < KG; ++q) {                                       \
+        _Pragma("clang loop unroll(full)") for (int i = 0; i < NLD; ++i) {                                 \
+            /* K and V: key (tid + 64*WAVES*i)/16 of tile q, dims (tid%16)*8 */                             \
+            const int ksrc = min((kb_) + q * KT + ((tid + 64 * WAVES * i) >> 4), it.k1 - 1);                \
+            kreg[q][i] = *reinterpret_cast<const u32x4 *>(Kg + (size_t)ksrc * HD + (tid & 15) * 8);         \
+            vreg[q][i] = *reinterpret_cast<const u32x4 *>(Vg + (size_t)ksrc * HD + (tid & 15) * 8);         \
+        }                                                                                                   \
     }
     KVR_ATT_FETCH(it.k0)
-    for (int kt = it.k0; kt < it.k1; kt += KT) {
+    for (int kb0 = it.k0; kb0 < it.k1; kb0 += KG * KT) {
         __syncthreads();
 #pragma clang loop unroll(full)
-        for (int i = 0; i < NLD; ++i) {
-            const int row = ((tid + 64 * WAVES * i) >> 4) * KS_STRIDE + (tid & 15) * 8;
-            *reinterpret_cast<u32x4 *>(&Ks[row]) = kreg[i];
-            *reinterpret_cast<u32x4 *>(&Vs[row]) = vreg[i];
+        for (int q = 0; q < KG; ++q) {
+#pragma clang loop unroll(full)
+            for (int i = 0; i < NLD; ++i) {
+                const int row = (q * KT + ((tid + 64 * WAVES * i) >> 4)) * KS_STRIDE + (tid & 15) * 8;
+                *reinterpret_cast<u32x4 *>(&Ks[row]) = kreg[q][i];
+                *reinterpret_cast<u32x4 *>(&Vs[row]) = vreg[q][i];
+            }
         }
         __syncthreads();
-        if (kt + KT < it.k1) {
-            KVR_ATT_FETCH(kt + KT)
+        if (kb0 + KG * KT < it.k1) {
+            KVR_ATT_FETCH(kb0 + KG * KT)
         }
+        const int kt = kb0 + kg * KT;  // this key group's tile
+        if (kt >= it.k1) continue;
+        const bf16_t *Kt = Ks + kg * KT * KS_STRIDE, *Vt = Vs + kg * KT * KS_STRIDE;
         const bool full = kt + KT <= it.k1 && kt + KT - 1 <= minpos;  // no key of the tile is masked
 
         // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the tile
@@ -150,7 +166,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         for (int nt = 0; nt < 4; ++nt) {
             bf16x8 kb[4];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kb[ks] = ld16(&Ks[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
+            for (int ks = 0; ks < 4; ++ks) kb[ks] = ld16(&Kt[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
 #pragma unroll
             for (int i = 0; i < PPW; ++i) {
                 s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -228,7 +244,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 // this lane addresses key ks*32 + 4g + m (then + 16), dims
                 // 16 nt + 4q .. +3, for m = (lane%16)/4, q = lane%4; it receives
                 // dim 16 nt + lane%16 of keys ks*32 + 4g + 0..3 and + 16 + 0..3
-                const bf16_t *vr = &Vs[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * KS_STRIDE + nt * 16 + 4 * (lane & 3)];
+                const bf16_t *vr = &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * KS_STRIDE + nt * 16 + 4 * (lane & 3)];
                 const i16x4 lo = lds_read_tr16(vr);
                 const i16x4 hi = lds_read_tr16(vr + 16 * KS_STRIDE);
                 va[ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -245,6 +261,43 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         }
     }
 #undef KVR_ATT_FETCH
+
+    if constexpr (KG == 2) {
+        // the second key group hands its state (per lane: O^T 32 values, m, l)
+        // to the wavefront of the first group that holds the same pairs
+        constexpr int ST = 34;
+        static_assert(WG * PPW * 64 * ST * 4 <= 2 * KG * KT * KS_STRIDE * 2, "merge area");
+        float *mg = reinterpret_cast<float *>(kv_lds);
+        __syncthreads();  // every wavefront is done with the K/V tiles
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                float *q = mg + ((lw * PPW + i) * 64 + lane) * ST;
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) q[nt * 4 + e] = oacc[i][nt][e];
+                q[32] = m[i];
+                q[33] = l[i];
+            }
+        }
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) {
+            const float *q = mg + ((lw * PPW + i) * 64 + lane) * ST;
+            const float m1 = q[32], l1 = q[33];
+            const float M = fmaxf(m[i], m1);
+            const float a0 = m[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[i] - M);
+            const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+            m[i] = M;
+            l[i] = l[i] * a0 + l1 * a1;
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) oacc[i][nt][e] = oacc[i][nt][e] * a0 + q[nt * 4 + e] * a1;
+        }
+    }
 
     // O^T accumulator: lane holds query row lane%16, dims 16*nt + 4*g + e
     const int rows_item = 16 * MT;
@@ -335,33 +388,37 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
 
 }  // namespace
 
-int attention_row_tiles(int Hq, int Hkv) {
+int attention_max_row_tiles(int Hq, int Hkv) {
     const int G = Hq / Hkv;
     return G >= 16 ? 1 : std::min(4, std::max(1, 16 / G));
 }
 
 hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows,
-                                 const AttnItem *items, int n_items, int layer, int Hq, int Hkv, float *part, bf16_t *O,
-                                 bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
+                                 const AttnItem *items, int n_items, int MT, int layer, int Hq, int Hkv, float *part,
+                                 bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
-    if (!Q_lo || !O_lo) return hipErrorInvalidValue;
-    const int MT = attention_row_tiles(Hq, Hkv);
-    const int ppw = ((Hq / Hkv) * MT + WAVES - 1) / WAVES;
-    if (ppw == 1)
-        kvr_launch(attention_mfma_kernel<1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items,
-                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
-    else if (ppw == 2)
-        kvr_launch(attention_mfma_kernel<2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items,
-                           layer, Hq, Hkv, MT, part, O, O_lo, (int)o_perm, lse);
+    if (!Q_lo || !O_lo || MT < 1 || MT > attention_max_row_tiles(Hq, Hkv)) return hipErrorInvalidValue;
+    // at most four pairs per item: two key groups of four wavefronts, one pair
+    // each; otherwise one group, pairs dealt round-robin to the eight wavefronts
+    const int npairs = (Hq / Hkv) * MT;
+    if (2 * npairs <= WAVES)
+        kvr_launch(attention_mfma_kernel<1, 2>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items, layer, Hq,
+                   Hkv, MT, part, O, O_lo, (int)o_perm, lse);
+    else if (npairs <= WAVES)
+        kvr_launch(attention_mfma_kernel<1, 1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items, layer, Hq,
+                   Hkv, MT, part, O, O_lo, (int)o_perm, lse);
+    else if (npairs <= 2 * WAVES)
+        kvr_launch(attention_mfma_kernel<2, 1>, dim3(n_items), dim3(64 * WAVES), 0, s, Q, Q_lo, rows, items, layer, Hq,
+                   Hkv, MT, part, O, O_lo, (int)o_perm, lse);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
-hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq, int Hkv,
-                                    bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
+hipError_t launch_attention_combine(const CombineItem *items, int n_items, int MT, const float *part, int Hq,
+                                    int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
-    const int MT = attention_row_tiles(Hq, Hkv);
+    if (MT < 1 || MT > attention_max_row_tiles(Hq, Hkv)) return hipErrorInvalidValue;
     kvr_launch(attention_combine_kernel<COMBINE_NP>, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part,
                Hq, Hkv, MT, O, O_lo, (int)o_perm, lse);
     return hipGetLastError();

@@ -175,13 +175,14 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
 hipError_t launch_attention_simple(bool bf16, const void *Q, const void *Q_lo, const RowInfo *rows,
                                    const DocInfo *docs, int R, int layer, int Hq, int Hkv, int hd, void *O, void *O_lo,
                                    bool o_perm, float *lse, hipStream_t s);
-// 16-row tiles per attention work item for a head grouping (items carry up to
-// 16 * this many rows).
-int attention_row_tiles(int Hq, int Hkv);
+// Largest number of 16-row tiles an attention work item may carry for a head
+// grouping.  A pass's items all carry at most MT tiles (1 <= MT <= this), the
+// same MT for the MFMA kernel and the combine (it sets the partials' layout).
+int attention_max_row_tiles(int Hq, int Hkv);
 hipError_t launch_attention_mfma(const bf16_t *Q, const bf16_t *Q_lo, const RowInfo *rows,
-                                 const AttnItem *items, int n_items, int layer, int Hq, int Hkv,
+                                 const AttnItem *items, int n_items, int MT, int layer, int Hq, int Hkv,
                                  float *part, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s);
-hipError_t launch_attention_combine(const CombineItem *items, int n_items, const float *part, int Hq,
+hipError_t launch_attention_combine(const CombineItem *items, int n_items, int MT, const float *part, int Hq,
                                     int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s);
 hipError_t launch_linear_simple(bool bf16, int epi, const LinearArgs &a, hipStream_t s);
 // Skinny MFMA path (R <= 64); nt = 16-row weight tiles per block (1..8).

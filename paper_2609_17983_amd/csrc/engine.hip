@@ -144,6 +144,7 @@ struct Tables {
     std::vector<DocInfo> docs;
     std::vector<AttnItem> items;
     std::vector<CombineItem> comb;
+    int att_mt = 1;  // 16-row tiles per attention item (rows of a row block / 16)
 };
 
 // Split the key ranges of the row blocks over work items: without splitting
@@ -156,23 +157,40 @@ struct Tables {
 void plan_attention(const kvr_ctx *c, Tables &t) {
     const int Hkv = c->d.n_kv_heads;
     const int G = c->d.n_heads / Hkv;
-    const int rows_blk = 16 * attention_row_tiles(c->d.n_heads, Hkv);
     struct Block { int doc, row0, nrows, kmax; };
     std::vector<Block> blocks;
-    for (int di = 0; di < (int)t.docs.size(); ++di) {
-        const DocInfo &dc = t.docs[di];
-        for (int b = 0; b < dc.nrows; b += rows_blk) {
-            const int nb = std::min(rows_blk, dc.nrows - b);
-            blocks.push_back({di, dc.row0 + b, nb, t.rows[dc.row0 + b + nb - 1].pos + 1});
+    auto make_blocks = [&](int rows_blk) {
+        blocks.clear();
+        for (int di = 0; di < (int)t.docs.size(); ++di) {
+            const DocInfo &dc = t.docs[di];
+            for (int b = 0; b < dc.nrows; b += rows_blk) {
+                const int nb = std::min(rows_blk, dc.nrows - b);
+                blocks.push_back({di, dc.row0 + b, nb, t.rows[dc.row0 + b + nb - 1].pos + 1});
+            }
         }
-    }
+    };
     const int target = env_int("KVR_ATT_TARGET", 256);
+    const int mt_max = attention_max_row_tiles(c->d.n_heads, Hkv);
+    int mt = mt_max;
+    make_blocks(16 * mt);
+    // Too few (row block, kv head) items to fill the GPU: split the key ranges.
+    // The row blocks then shrink to one 16-row tile: the items of a key range
+    // read the same K/V tiles (from L2), each row's keys are cut into fewer
+    // parts (fewer partials to write and combine), and an item of one tile
+    // has few enough (head, row tile) pairs for the kernel's two key groups.
+    const bool split = (long long)blocks.size() * Hkv < target / 2;
+    if (split) {
+        mt = std::min(mt_max, std::max(1, env_int("KVR_ATT_MT", 1)));
+        make_blocks(16 * mt);
+    }
+    t.att_mt = mt;
+    const int rows_blk = 16 * mt;
     long long total_keys = 0;
     for (auto &b : blocks) total_keys += b.kmax;
     int KS = 1 << 30;
     const size_t slot_floats = (size_t)G * rows_blk * PART_ROW;
     const size_t max_slots = c->attn_part_floats / slot_floats;
-    if ((long long)blocks.size() * Hkv < target / 2) {
+    if (split) {
         long long ks = (total_keys * Hkv + target - 1) / target;
         ks = std::max<long long>(env_int("KVR_ATT_MINKS", 128), (ks + ATT_KT - 1) / ATT_KT * ATT_KT);
         for (;; ks *= 2) {
@@ -429,11 +447,11 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
         float *lse = mh ? mh->lse : nullptr;
         if (attn_mfma) {
             KVR_CHECK(launch_attention_mfma((const bf16_t *)c->Qb, (const bf16_t *)c->Qb_lo, rows, items,
-                                            (int)t.items.size(), l, d.n_heads, d.n_kv_heads, c->attn_part,
+                                            (int)t.items.size(), t.att_mt, l, d.n_heads, d.n_kv_heads, c->attn_part,
                                             (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, op, lse, s),
                       "attention", ST_ATTN);
             if (!t.comb.empty())
-                KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), c->attn_part, d.n_heads, d.n_kv_heads,
+                KVR_CHECK(launch_attention_combine(comb, (int)t.comb.size(), t.att_mt, c->attn_part, d.n_heads, d.n_kv_heads,
                                                    (bf16_t *)c->Ob, (bf16_t *)c->Ob_lo, op, lse, s), "attention_combine", ST_COMBINE);
         } else {
             KVR_CHECK(launch_attention_simple(bf, c->Qb, c->Qb_lo, rows, docs, R, l, d.n_heads, d.n_kv_heads, hd, c->Ob,
