@@ -21,6 +21,21 @@ __host__ __device__ __forceinline__ size_t perm_offset(int r, int c, int K) {
     return ((size_t)((r >> 4) * (K >> 5) + (c >> 5)) * 64 + (r & 15) + 16 * ((c & 31) >> 3)) * 8 + (c & 7);
 }
 
+// Packed weights (pack.hip): the matrix is a sequence of 16-row tiles; each
+// tile's k-step is one 1 KB operand fragment.  The tiles are stored in groups
+// of `grp` consecutive tiles (the last group may be shorter), k-step major
+// within a group, so a block that streams the tiles of one group reads one
+// contiguous range.  Element offset of tile t's fragment at k-step 0; the
+// fragment of k-step s is `*kstride` elements further on.  grp <= 1 is
+// tile-major (each tile's k-steps adjacent).
+__host__ __device__ __forceinline__ size_t packed_tile_offset(int t, int ntiles, int ksteps, int grp, int *kstride) {
+    const int g = grp > 1 ? grp : 1;
+    const int g0 = (t / g) * g;
+    const int gl = ntiles - g0 < g ? ntiles - g0 : g;
+    *kstride = gl * 512;
+    return ((size_t)g0 * ksteps + (t - g0)) * 512;
+}
+
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
 // fp32 -> bf16, round to nearest, ties to even (NaN kept quiet).
@@ -111,6 +126,7 @@ struct LinearArgs {
     const void *w[3];     // row-major row blocks of W (simple kernel)
     int32_t seg_end[3];   // cumulative output-column boundaries of the blocks
     const void *wp;       // W packed in operand order (tiled kernel; pack.hip)
+    int32_t grp;          // tile group of the packed layout (packed_tile_offset)
     void *out;            // STORE: float [R][ldo]; RESID: float [R][ldo] (+=);
                           // SWIGLU: operand type [R][ldo]
     void *out_lo;         // SWIGLU: low part of the compensated output, or null
@@ -128,6 +144,7 @@ struct SkinnyArgs {
     int32_t R, K, N;      // N: output columns (SWIGLU: number of features)
     const void *w;         // packed weight
     int32_t ntiles;
+    int32_t grp;           // tile group of the packed layout (packed_tile_offset)
     void *out, *out_lo;    // SWIGLU writes a compensated pair
     int32_t split;
 };
@@ -197,7 +214,7 @@ int tiled_blocks(int R, int vrows, int *slots);
 // the virtual matrix; interleave: w0 = gate, w1 = up, tile t = gate rows
 // 8t..8t+7 then up rows 8t..8t+7) of K columns into operand order at dst.
 hipError_t launch_pack_weight(const void *w0, const void *w1, const void *w2, int e0, int e1, bool interleave,
-                              int V, int K, void *dst, hipStream_t s);
+                              int V, int K, int grp, void *dst, hipStream_t s);
 
 // Scoring rows: hidden rows Y [R][d] fp32 -> LM-head operand (compensated
 // bf16 pair, operand order or row-major, or fp32 row-major).

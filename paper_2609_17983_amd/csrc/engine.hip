@@ -43,6 +43,7 @@ struct kvr_ctx {
 
     // projection weights repacked in operand order (bf16 MFMA paths)
     struct PackedLayer { const void *qkv, *o, *gu, *down; };
+    int gu_grp = 1;  // tile group of the packed gate/up weights (packed_tile_offset)
     std::vector<PackedLayer> pk;
     char *wpk = nullptr;
     size_t wpk_bytes = 0;
@@ -110,7 +111,7 @@ constexpr int SCORE_ROWS = 64;  // rows per LM-head launch (the skinny kernel's 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 int env_int(const char *name, int dflt) {
-    const char *v = getenv(name);
+    const char *v = name ? getenv(name) : nullptr;
     return (v && *v) ? atoi(v) : dflt;
 }
 
@@ -292,16 +293,18 @@ LinearArgs make_args(const void *x, const void *x_lo, int ldx, int R, int K, int
     a.w[0] = w0; a.w[1] = w1; a.w[2] = w2;
     a.seg_end[0] = e0; a.seg_end[1] = e1; a.seg_end[2] = N;
     a.wp = wp;
+    a.grp = 1;
     a.out = out; a.ldo = ldo;
     a.split = 1;
     return a;
 }
 
-hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *wp, void *out,
+hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *wp, int grp, void *out,
                   void *out_lo, const SkinnyPlan &p, hipStream_t s) {
     SkinnyArgs a{};
     a.x = x; a.x_lo = x_lo; a.R = R; a.K = K; a.N = N;
     a.w = wp;
+    a.grp = grp;
     a.ntiles = (epi == EPI_SWIGLU ? 2 * N : N) / 16;
     a.out = out; a.out_lo = out_lo; a.split = p.split;
     return launch_linear_skinny(epi, a, p.nt, s);
@@ -431,7 +434,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                   "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, c->P, nullptr, p_qkv, s), "qkv",
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, 1, c->P, nullptr, p_qkv, s), "qkv",
                       ST_QKV);
             qkv_split = p_qkv.split;
         } else {
@@ -465,7 +468,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             if (l == d.n_layers - 1) return KVR_OK;
         }
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
+            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, 1, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
             resid_split = p_o.split;
         } else if (pw.o) {
             // packed: partial tiles into P (the next RMSNorm adds them to H)
@@ -481,15 +484,16 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                   "rmsnorm(mlp)", ST_NORM);
         resid_split = 0;
         if (sk) {
-            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
+            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->gu_grp, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
                       ST_GATEUP);
-            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, c->P, nullptr, p_down, s), "down",
+            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, 1, c->P, nullptr, p_down, s), "down",
                       ST_DOWN);
             resid_split = p_down.split;
         } else {
-            KVR_CHECK(linear(c, EPI_SWIGLU, make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu,
-                                                  c->Ab, c->Ab_lo, F), s),
-                      "gate_up", ST_GATEUP);
+            LinearArgs ga = make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu, c->Ab,
+                                      c->Ab_lo, F);
+            ga.grp = c->gu_grp;
+            KVR_CHECK(linear(c, EPI_SWIGLU, ga, s), "gate_up", ST_GATEUP);
             if (pw.down) {
                 LinearArgs a = make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down, c->P,
                                          nullptr, D);
@@ -538,7 +542,7 @@ kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t 
         int nsplit = 1;
         if (c->lm_pk) {
             KVR_SCHECK(launch_to_operand(true, true, Y, R, D, c->Xn, c->Xn_lo, s), "lm_head operand", ST_LMHEAD);
-            KVR_SCHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, V, c->lm_pk, c->score_part, nullptr, plan, s),
+            KVR_SCHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, V, c->lm_pk, 1, c->score_part, nullptr, plan, s),
                        "lm_head", ST_LMHEAD);
             nsplit = plan.split;
         } else if (c->bf16) {
@@ -727,28 +731,34 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
             return fail(nullptr, KVR_E_NOMEM, "kvr_create: packed weight allocation failed");
         }
         c->pk.resize(d.n_layers);
+        // gate/up tiles are stored in groups of the tile count a skinny block
+        // streams (the plan for a repair of up to 64 rows), so that each block
+        // reads one contiguous range; the other projections split K over
+        // blocks and gain nothing from it
+        c->gu_grp = plan_skinny(2 * F / 16, D, std::min(64, std::max(1, d.max_rows)), true, 16, nullptr, nullptr).nt;
         bf16_t *dst = (bf16_t *)c->wpk;
         for (int l = 0; l < d.n_layers && e == hipSuccess; ++l) {
             const kvr_layer_weights &w = c->layers[l];
             kvr_ctx::PackedLayer &pl = c->pk[l];
             pl.qkv = dst;
-            e = launch_pack_weight(w.wq, w.wk, w.wv, qd, qd + kd, false, NQKV, D, dst, 0);
+            e = launch_pack_weight(w.wq, w.wk, w.wv, qd, qd + kd, false, NQKV, D, 1, dst, 0);
             dst += (size_t)NQKV * D;
             pl.o = dst;
-            if (e == hipSuccess) e = launch_pack_weight(w.wo, w.wo, w.wo, D, D, false, D, qd, dst, 0);
+            if (e == hipSuccess) e = launch_pack_weight(w.wo, w.wo, w.wo, D, D, false, D, qd, 1, dst, 0);
             dst += (size_t)D * qd;
             pl.gu = dst;
-            if (e == hipSuccess) e = launch_pack_weight(w.w_gate, w.w_up, w.w_up, F, 2 * F, true, 2 * F, D, dst, 0);
+            if (e == hipSuccess)
+                e = launch_pack_weight(w.w_gate, w.w_up, w.w_up, F, 2 * F, true, 2 * F, D, c->gu_grp, dst, 0);
             dst += (size_t)2 * F * D;
             pl.down = dst;
-            if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, dst, 0);
+            if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, 1, dst, 0);
             dst += (size_t)D * F;
         }
         if (e == hipSuccess && d.vocab % 16 == 0) {
             c->lm_pk_bytes = (size_t)d.vocab * D * 2;
             e = hipMalloc(&c->lm_pk, c->lm_pk_bytes);
             if (e == hipSuccess) e = launch_pack_weight(c->lm_head, c->lm_head, c->lm_head, d.vocab, d.vocab, false,
-                                                        d.vocab, D, c->lm_pk, 0);
+                                                        d.vocab, D, 1, c->lm_pk, 0);
         }
         if (e == hipSuccess) e = hipStreamSynchronize(0);
         if (e != hipSuccess) {

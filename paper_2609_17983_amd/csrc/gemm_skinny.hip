@@ -58,9 +58,11 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     // tiles past the end (last block of a ragged grid) re-read the last tile;
     // their results are never stored
     const bf16_t *wp[NT];
+    int wstride[NT];  // elements between a tile's k-steps (packed_tile_offset)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
-        wp[nt] = (const bf16_t *)a.w + ((size_t)min(tg * NT + nt, a.ntiles - 1) * ksteps * 64 + lane) * 8;
+        wp[nt] = (const bf16_t *)a.w +
+                 packed_tile_offset(min(tg * NT + nt, a.ntiles - 1), a.ntiles, ksteps, a.grp, &wstride[nt]) + lane * 8;
     const bf16_t *xp[MT], *xq[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -81,7 +83,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         // compiler can count outstanding loads exactly.
         auto load = [&](int j, int st) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) wv[j][nt] = ld16_stream(wp[nt] + (size_t)st * 512);
+            for (int nt = 0; nt < NT; ++nt) wv[j][nt] = ld16_stream(wp[nt] + (size_t)st * wstride[nt]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 xv[j][mt] = ld16(xp[mt] + (size_t)st * 512);

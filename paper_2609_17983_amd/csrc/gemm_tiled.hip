@@ -109,22 +109,24 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
     // the lambda below, made the host compiler drop the kernel's launch stub.
     static_assert(FPW <= 8, "at most eight fragments per wavefront");
     const bf16_t *src[8];
+    int kstride[8];  // elements between a fragment's k-steps
 #pragma unroll
     for (int i = 0; i < FPW; ++i) {
         const int f = FPW * w + i;
         if (f < 2 * RT) {
             const int t = min(bm * RT + (f % RT), rtiles - 1);
             src[i] = (const bf16_t *)(f < RT ? a.x : a.x_lo) + ((size_t)t * ksteps * 64 + lane) * 8;
+            kstride[i] = 512;
         } else {
             const int t = min(bn * WT + (f - 2 * RT), ntiles - 1);
-            src[i] = (const bf16_t *)a.wp + ((size_t)t * ksteps * 64 + lane) * 8;
+            src[i] = (const bf16_t *)a.wp + packed_tile_offset(t, ntiles, ksteps, a.grp, &kstride[i]) + lane * 8;
         }
     }
     auto issue = [&](int kk) {
         bf16_t *st = lds + (kk % STAGES) * STAGE + FPW * w * FRAG;
 #pragma unroll
         for (int i = 0; i < FPW; ++i)
-            __builtin_amdgcn_global_load_lds(src[i] + (size_t)(k0 + kk) * 512, st + i * FRAG, 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(src[i] + (size_t)(k0 + kk) * kstride[i], st + i * FRAG, 16, 0, 0);
     };
 
     f32x4 acc[4][JT];

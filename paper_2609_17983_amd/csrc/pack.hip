@@ -15,6 +15,9 @@
 //   * gate/up interleave: 16-row tile t holds gate rows 8t..8t+7 followed by
 //     up rows 8t..8t+7, so both halves of SwiGLU feature f sit in the same
 //     tile, eight columns apart.
+// The tiles are stored in groups of `grp` (packed_tile_offset): a skinny
+// block that owns one group then streams one contiguous range instead of grp
+// separate ones (gate/up of the 8B shape at 48 rows: 47.8 -> 44.5 us).
 #include <algorithm>
 
 #include "common.h"
@@ -25,7 +28,7 @@ namespace {
 
 __global__ __launch_bounds__(256) void pack_weight_kernel(const bf16_t *w0, const bf16_t *w1, const bf16_t *w2,
                                                           int e0, int e1, int interleave, int V, int K,
-                                                          bf16_t *dst) {
+                                                          int grp, bf16_t *dst) {
     const int ksteps = K >> 5;
     const size_t chunks = (size_t)V * K / 8;  // 16-byte chunks of the packed matrix
     for (size_t q = blockIdx.x * (size_t)blockDim.x + threadIdx.x; q < chunks; q += (size_t)gridDim.x * blockDim.x) {
@@ -45,19 +48,21 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const bf16_t *w0, cons
         } else {
             src = w2 + (size_t)(v - e1) * K;
         }
-        *reinterpret_cast<u32x4 *>(dst + q * 8) = *reinterpret_cast<const u32x4 *>(src + k);
+        int kstride;
+        const size_t o = packed_tile_offset(t, V >> 4, ksteps, grp, &kstride) + (size_t)s * kstride + lane * 8;
+        *reinterpret_cast<u32x4 *>(dst + o) = *reinterpret_cast<const u32x4 *>(src + k);
     }
 }
 
 }  // namespace
 
 hipError_t launch_pack_weight(const void *w0, const void *w1, const void *w2, int e0, int e1, bool interleave,
-                              int V, int K, void *dst, hipStream_t s) {
-    if (V <= 0 || V % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+                              int V, int K, int grp, void *dst, hipStream_t s) {
+    if (V <= 0 || V % 16 != 0 || K % 32 != 0 || grp < 1) return hipErrorInvalidValue;
     const size_t chunks = (size_t)V * K / 8;
     const int grid = (int)std::min<size_t>((chunks + 255) / 256, 65536);
     kvr_launch(pack_weight_kernel, dim3(grid), dim3(256), 0, s, (const bf16_t *)w0, (const bf16_t *)w1,
-                       (const bf16_t *)w2, e0, e1, interleave ? 1 : 0, V, K, (bf16_t *)dst);
+                       (const bf16_t *)w2, e0, e1, interleave ? 1 : 0, V, K, grp, (bf16_t *)dst);
     return hipGetLastError();
 }
 
