@@ -244,6 +244,106 @@ __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, in
     }
 }
 
+// Four values of row-major type T at p (8-byte or 16-byte store).
+template <typename T>
+__device__ __forceinline__ void store4(T *p, float4 v) {
+    if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<float4 *>(p) = v;
+    } else {
+        const uint32_t a = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+        const uint32_t b = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+        *reinterpret_cast<uint2 *>(p) = make_uint2(a, b);
+    }
+}
+// Four consecutive operand values (store_operand for each, vectorised).
+template <typename T>
+__device__ __forceinline__ void store4_operand(T *hi, T *lo, size_t i, float4 v) {
+    if constexpr (sizeof(T) == 4) {
+        store4(hi + i, v);
+    } else {
+        const bf16_t h[4] = {f32_to_bf16(v.x), f32_to_bf16(v.y), f32_to_bf16(v.z), f32_to_bf16(v.w)};
+        *reinterpret_cast<uint2 *>(hi + i) =
+            make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+        if (lo) {
+            const float4 d = {v.x - bf16_to_f32(h[0]), v.y - bf16_to_f32(h[1]), v.z - bf16_to_f32(h[2]),
+                              v.w - bf16_to_f32(h[3])};
+            store4(lo + i, d);
+        }
+    }
+}
+template <typename T>
+__device__ __forceinline__ float4 load4_f32(const T *p) {
+    if constexpr (sizeof(T) == 4) return *reinterpret_cast<const float4 *>(p);
+    else return float4{to_f32(p[0]), to_f32(p[1]), to_f32(p[2]), to_f32(p[3])};
+}
+
+// The same as rope_scatter_kernel with one thread per (row, head, four
+// rotary pairs) and per (row, four value dimensions): nothing in it is
+// reduced over a row, so the work spreads over all compute units instead of
+// one block per row (head_dim a multiple of 8).
+template <typename T>
+__global__ __launch_bounds__(256) void rope_scatter_vec_kernel(const float *qkv, int nsplit, int R, const T *bq,
+                                                               const T *bk, const T *bv, const RowInfo *rows,
+                                                               const DocInfo *docs, int layer, int Hq, int Hkv, int hd,
+                                                               const float *rcos, const float *rsin, T *Q, T *Q_lo) {
+    const int r = blockIdx.x;
+    const int idx = blockIdx.y * 256 + threadIdx.x;
+    const int half = hd >> 1, hq4 = half >> 2;
+    const int qd = Hq * hd, kd = Hkv * hd;
+    const int N = qd + 2 * kd;
+    const int nrot = (Hq + Hkv) * hq4;
+    if (idx >= nrot + (kd >> 2)) return;
+    const RowInfo ri = rows[r];
+    const DocInfo dc = docs[ri.doc];
+    // columns c..c+3 of this row, the split-K partial tiles summed in order
+    auto load4 = [&](int c) {
+        float4 v = *reinterpret_cast<const float4 *>(qkv + (size_t)r * N + c);
+        for (int q = 1; q < nsplit; ++q) {
+            const float4 p = *reinterpret_cast<const float4 *>(qkv + ((size_t)q * R + r) * N + c);
+            v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+        }
+        return v;
+    };
+    T *cache = (T *)dc.cache;
+    const size_t head_stride = (size_t)dc.n_cap * hd;
+    if (idx < nrot) {
+        const int j = idx / hq4, i = (idx - j * hq4) * 4;
+        const bool isq = j < Hq;
+        const int g = j - Hq;
+        const int ca = isq ? j * hd + i : qd + g * hd + i;
+        float4 a = load4(ca), b = load4(ca + half);
+        const T *bias = isq ? bq : bk;
+        if (bias) {
+            const int bo = (isq ? j : g) * hd + i;
+            const float4 ba = load4_f32(bias + bo), bb = load4_f32(bias + bo + half);
+            a.x += ba.x; a.y += ba.y; a.z += ba.z; a.w += ba.w;
+            b.x += bb.x; b.y += bb.y; b.z += bb.z; b.w += bb.w;
+        }
+        const float4 c = *reinterpret_cast<const float4 *>(rcos + (size_t)ri.pos * half + i);
+        const float4 sn = *reinterpret_cast<const float4 *>(rsin + (size_t)ri.pos * half + i);
+        const float4 o1 = {a.x * c.x - b.x * sn.x, a.y * c.y - b.y * sn.y, a.z * c.z - b.z * sn.z, a.w * c.w - b.w * sn.w};
+        const float4 o2 = {b.x * c.x + a.x * sn.x, b.y * c.y + a.y * sn.y, b.z * c.z + a.z * sn.z, b.w * c.w + a.w * sn.w};
+        if (isq) {
+            store4_operand(Q, Q_lo, (size_t)r * qd + j * hd + i, o1);
+            store4_operand(Q, Q_lo, (size_t)r * qd + j * hd + i + half, o2);
+        } else {
+            T *kb = cache + (((size_t)layer * 2 + 0) * Hkv + g) * head_stride + (size_t)ri.pos * hd;
+            store4(kb + i, o1);
+            store4(kb + i + half, o2);
+        }
+    } else {
+        const int c4 = (idx - nrot) * 4;  // column of the value part [0, kd)
+        float4 v = load4(qd + kd + c4);
+        if (bv) {
+            const float4 bb = load4_f32(bv + c4);
+            v.x += bb.x; v.y += bb.y; v.z += bb.z; v.w += bb.w;
+        }
+        const int g = c4 / hd, i = c4 - g * hd;
+        T *vb = cache + (((size_t)layer * 2 + 1) * Hkv + g) * head_stride + (size_t)ri.pos * hd;
+        store4(vb + i, v);
+    }
+}
+
 // One wavefront per (row, query head): online softmax over keys 0..pos.
 // When `lse` is given, lse[r * Hq + j] = log2 of the softmax normaliser of the
 // scores q.k * log2(e)/sqrt(hd) (the base-2 log-sum-exp).
@@ -420,6 +520,19 @@ hipError_t launch_rope_scatter(bool bf16, const float *qkv, int nsplit, const vo
                                int Hkv, int hd, const float *rope_cos, const float *rope_sin, void *Q, void *Q_lo,
                                hipStream_t s) {
     if (R <= 0) return hipSuccess;
+    if (hd % 8 == 0) {
+        const int work = (Hq + Hkv) * (hd / 8) + Hkv * hd / 4;  // threads per row
+        const dim3 grid(R, (work + 255) / 256);
+        if (bf16)
+            kvr_launch(rope_scatter_vec_kernel<bf16_t>, grid, dim3(256), 0, s, qkv, nsplit, R, (const bf16_t *)bq,
+                       (const bf16_t *)bk, (const bf16_t *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
+                       (bf16_t *)Q, (bf16_t *)Q_lo);
+        else
+            kvr_launch(rope_scatter_vec_kernel<float>, grid, dim3(256), 0, s, qkv, nsplit, R, (const float *)bq,
+                       (const float *)bk, (const float *)bv, rows, docs, layer, Hq, Hkv, hd, rope_cos, rope_sin,
+                       (float *)Q, (float *)nullptr);
+        return hipGetLastError();
+    }
     const size_t lds = (size_t)(Hq + 2 * Hkv) * hd * sizeof(float);
     if (lds > 160 * 1024 || ((Hq + 2 * Hkv) * hd) % 4 != 0) return hipErrorInvalidValue;
     if (bf16)
