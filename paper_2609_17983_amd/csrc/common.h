@@ -147,6 +147,11 @@ struct SkinnyArgs {
     int32_t grp;           // tile group of the packed layout (packed_tile_offset)
     void *out, *out_lo;    // SWIGLU writes a compensated pair
     int32_t split;
+    // RMS scale of the rows (resid_gain): when rs_ssq is set, output row r is
+    // multiplied by rsqrt((rs_ssq[0][r] + ... + rs_ssq[rs_nb-1][r]) / rs_d + rs_eps)
+    const float *rs_ssq;
+    int32_t rs_nb, rs_d;
+    float rs_eps;
 };
 
 // ---- kernel launch with optional execution timing
@@ -178,6 +183,12 @@ hipError_t launch_embed(bool bf16, const RowInfo *rows, const DocInfo *docs, int
 // row-major with stride ldx, or in operand order when `perm`.
 hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
                           int R, int d, float eps, void *X, void *X_lo, int ldx, bool perm, hipStream_t s);
+// Residual update + gain for the skinny path (see resid_gain_kernel): H[r] +=
+// partials, X = H * gain (compensated, operand order), ssq[b][r] per 1024-column
+// block b; resid_gain_blocks(d) blocks per row.
+int resid_gain_blocks(int d);
+hipError_t launch_resid_gain(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain, int R, int d,
+                             void *X, void *X_lo, float *ssq, hipStream_t s);
 hipError_t launch_final_norm(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain,
                              const RowInfo *rows, const DocInfo *docs, int R, int d, float eps, hipStream_t s);
 // qkv: `nsplit` fp32 tiles [nsplit][R][qd+2kd] summed in order.

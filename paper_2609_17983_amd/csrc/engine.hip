@@ -67,6 +67,7 @@ struct kvr_ctx {
     char *ws = nullptr;
     size_t ws_bytes = 0;
     float *H = nullptr, *P = nullptr;  // residual stream; projection outputs / split-K partials
+    float *rs_ssq = nullptr;           // skinny passes: per-row sums of squares by column block (resid_gain)
     size_t p_floats = 0;               // capacity of P
     // matrix operands; in bf16 each is a compensated pair (hi, lo)
     void *Xn = nullptr, *Qb = nullptr, *Ob = nullptr, *Ab = nullptr;
@@ -299,12 +300,19 @@ LinearArgs make_args(const void *x, const void *x_lo, int ldx, int R, int K, int
     return a;
 }
 
+// rs_ssq: the rows' sums of squares from resid_gain (X is H * gain, not yet
+// normalised): the kernel applies the RMS scale to its output rows.
 hipError_t skinny(int epi, const void *x, const void *x_lo, int R, int K, int N, const void *wp, int grp, void *out,
-                  void *out_lo, const SkinnyPlan &p, hipStream_t s) {
+                  void *out_lo, const SkinnyPlan &p, hipStream_t s, const float *rs_ssq = nullptr,
+                  float rs_eps = 0.f) {
     SkinnyArgs a{};
     a.x = x; a.x_lo = x_lo; a.R = R; a.K = K; a.N = N;
     a.w = wp;
     a.grp = grp;
+    a.rs_ssq = rs_ssq;
+    a.rs_nb = resid_gain_blocks(K);
+    a.rs_d = K;
+    a.rs_eps = rs_eps;
     a.ntiles = (epi == EPI_SWIGLU ? 2 * N : N) / 16;
     a.out = out; a.out_lo = out_lo; a.split = p.split;
     return launch_linear_skinny(epi, a, p.nt, s);
@@ -430,12 +438,19 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     for (int l = 0; l < n_run; ++l) {
         const kvr_layer_weights &w = c->layers[l];
         const kvr_ctx::PackedLayer pw = c->wpk ? c->pk[l] : kvr_ctx::PackedLayer{nullptr, nullptr, nullptr, nullptr};
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, op, s),
-                  "rmsnorm(attn)", ST_NORM);
+        // skinny passes: the projections apply the RMS scale to their outputs
+        if (sk)
+            KVR_CHECK(launch_resid_gain(bf, c->H, c->P, resid_split, w.attn_norm, R, D, c->Xn, c->Xn_lo, c->rs_ssq, s),
+                      "rmsnorm(attn)", ST_NORM);
+        else
+            KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.attn_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D,
+                                     op, s),
+                      "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, 1, c->P, nullptr, p_qkv, s), "qkv",
-                      ST_QKV);
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, 1, c->P, nullptr, p_qkv, s, c->rs_ssq,
+                             d.rms_eps),
+                      "qkv", ST_QKV);
             qkv_split = p_qkv.split;
         } else {
             LinearArgs a = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr,
@@ -480,12 +495,18 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
         }
-        KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, op, s),
-                  "rmsnorm(mlp)", ST_NORM);
+        if (sk)
+            KVR_CHECK(launch_resid_gain(bf, c->H, c->P, resid_split, w.mlp_norm, R, D, c->Xn, c->Xn_lo, c->rs_ssq, s),
+                      "rmsnorm(mlp)", ST_NORM);
+        else
+            KVR_CHECK(launch_rmsnorm(bf, bf, c->H, c->P, resid_split, w.mlp_norm, R, D, d.rms_eps, c->Xn, c->Xn_lo, D, op,
+                                     s),
+                      "rmsnorm(mlp)", ST_NORM);
         resid_split = 0;
         if (sk) {
-            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->gu_grp, c->Ab, c->Ab_lo, p_gu, s), "gate_up",
-                      ST_GATEUP);
+            KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->gu_grp, c->Ab, c->Ab_lo, p_gu, s, c->rs_ssq,
+                             d.rms_eps),
+                      "gate_up", ST_GATEUP);
             KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, 1, c->P, nullptr, p_down, s), "down",
                       ST_DOWN);
             resid_split = p_down.split;
@@ -673,7 +694,8 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
                  o_Xl = take(R * D * lo_es), o_Ql = take(R * qd * lo_es), o_Ol = take(R * qd * lo_es),
                  o_Al = take(R * F * lo_es),
                  o_cos = take((size_t)d.max_ctx * (hd / 2) * 4), o_sin = take((size_t)d.max_ctx * (hd / 2) * 4),
-                 o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes);
+                 o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes),
+                 o_ss = take((size_t)64 * resid_gain_blocks(D) * 4);
     c->ws_bytes = off;
     e = hipMalloc((void **)&c->ws, c->ws_bytes);
     if (e != hipSuccess) { delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: workspace allocation failed"); }
@@ -694,6 +716,7 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     c->rope_sin = (float *)(c->ws + o_sin);
     c->attn_part = (float *)(c->ws + o_ap);
     c->d_tables = c->ws + o_tab;
+    c->rs_ssq = (float *)(c->ws + o_ss);
 
     e = hipHostMalloc((void **)&c->h_stage, c->tables_bytes, hipHostMallocDefault);
     if (e != hipSuccess) { (void)hipFree(c->ws); delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: pinned staging allocation failed"); }

@@ -125,6 +125,17 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
             for (int e = 0; e < 4; ++e) red[w][(mt * 16 + 4 * (lane >> 4) + e) * LD + nt * 16 + (lane & 15)] = acc[mt][nt][e];
+    // row scales (RMSNorm applied to the output, see SkinnyArgs)
+    __shared__ float rscale[MT * 16];
+    if (threadIdx.x < MT * 16) {
+        float sc = 1.f;
+        if (a.rs_ssq && (int)threadIdx.x < a.R) {
+            float t = 0.f;
+            for (int b = 0; b < a.rs_nb; ++b) t += a.rs_ssq[(size_t)b * a.R + threadIdx.x];
+            sc = rsqrtf(t / (float)a.rs_d + a.rs_eps);
+        }
+        rscale[threadIdx.x] = sc;
+    }
     __syncthreads();
     auto total4 = [&](int r, int c) {
         const int i = r * LD + c;
@@ -144,8 +155,9 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         for (int i = threadIdx.x; i < MT * 16 * NT; i += 256) {
             const int r = i / NT, nt = i - r * NT;
             if (r >= R || nt >= tiles_here) continue;
-            const f32x4 g0 = total4(r, 16 * nt), g1 = total4(r, 16 * nt + 4);
-            const f32x4 u0 = total4(r, 16 * nt + 8), u1 = total4(r, 16 * nt + 12);
+            const float sc = rscale[r];
+            const f32x4 g0 = total4(r, 16 * nt) * sc, g1 = total4(r, 16 * nt + 4) * sc;
+            const f32x4 u0 = total4(r, 16 * nt + 8) * sc, u1 = total4(r, 16 * nt + 12) * sc;
             float y[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -170,7 +182,7 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
         for (int i = threadIdx.x; i < MT * 16 * C4; i += 256) {
             const int r = i / C4, c = 4 * (i - r * C4);
             if (r >= R || c >= 16 * tiles_here) continue;
-            *reinterpret_cast<f32x4 *>(out + (size_t)r * a.N + c) = total4(r, c);
+            *reinterpret_cast<f32x4 *>(out + (size_t)r * a.N + c) = total4(r, c) * rscale[r];
         }
     }
 }

@@ -244,6 +244,46 @@ __global__ __launch_bounds__(1024) void rope_scatter_kernel(const float *qkv, in
     }
 }
 
+// Residual update for a pass whose projections apply the RMS scale to their
+// outputs (the skinny path): H[r] += the `nsplit` partial tiles (in order),
+// X = H * gain as a compensated operand in operand order, and ssq[b][r] = the
+// sum of H[r][c]^2 over the 1024 columns of column block b (fixed reduction
+// order).  RMSNorm's scale is one factor per row and the projection is
+// linear, so the projection that reads X multiplies its output row r by
+// rsqrt((ssq[0][r] + ... ) / d + eps) instead; the work then spreads over
+// (row, column block) blocks rather than one block per row.
+template <typename G>
+__global__ __launch_bounds__(256) void resid_gain_kernel(float *H, const float *part, int nsplit, int R, const G *gain,
+                                                         int d, bf16_t *X, bf16_t *X_lo, float *ssq) {
+    __shared__ float red[4];
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int i = b * 256 + threadIdx.x;  // float4 index within the row
+    float ss = 0.f;
+    if (4 * i < d) {
+        float *hp = H + (size_t)r * d + 4 * i;
+        float4 h = *reinterpret_cast<const float4 *>(hp);
+        if (nsplit) {
+            h = add_partials(h, part, nsplit, R, r, d, i);
+            *reinterpret_cast<float4 *>(hp) = h;
+        }
+        ss = h.x * h.x + h.y * h.y + h.z * h.z + h.w * h.w;
+        const float4 x = {h.x * to_f32(gain[4 * i]), h.y * to_f32(gain[4 * i + 1]), h.z * to_f32(gain[4 * i + 2]),
+                          h.w * to_f32(gain[4 * i + 3])};
+        const bf16_t hi[4] = {f32_to_bf16(x.x), f32_to_bf16(x.y), f32_to_bf16(x.z), f32_to_bf16(x.w)};
+        const bf16_t lo[4] = {f32_to_bf16(x.x - bf16_to_f32(hi[0])), f32_to_bf16(x.y - bf16_to_f32(hi[1])),
+                              f32_to_bf16(x.z - bf16_to_f32(hi[2])), f32_to_bf16(x.w - bf16_to_f32(hi[3]))};
+        const size_t o = perm_offset(r, 4 * i, d);  // four consecutive columns are adjacent in operand order
+        *reinterpret_cast<uint2 *>(X + o) =
+            make_uint2((uint32_t)hi[0] | ((uint32_t)hi[1] << 16), (uint32_t)hi[2] | ((uint32_t)hi[3] << 16));
+        *reinterpret_cast<uint2 *>(X_lo + o) =
+            make_uint2((uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16));
+    }
+    ss = warp_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    if (threadIdx.x == 0) ssq[(size_t)b * R + r] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
 // Four values of row-major type T at p (8-byte or 16-byte store).
 template <typename T>
 __device__ __forceinline__ void store4(T *p, float4 v) {
@@ -499,6 +539,22 @@ hipError_t launch_rmsnorm(bool bf16_out, bool bf16_gain, float *H, const float *
     } else {
         return hipErrorInvalidValue;
     }
+    return hipGetLastError();
+}
+
+int resid_gain_blocks(int d) { return (d + 1023) / 1024; }
+
+hipError_t launch_resid_gain(bool bf16_gain, float *H, const float *part, int nsplit, const void *gain, int R, int d,
+                             void *X, void *X_lo, float *ssq, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (d % 32 != 0 || !X || !X_lo || !ssq) return hipErrorInvalidValue;
+    const dim3 grid(R, resid_gain_blocks(d));
+    if (bf16_gain)
+        kvr_launch(resid_gain_kernel<bf16_t>, grid, dim3(256), 0, s, H, part, nsplit, R, (const bf16_t *)gain, d,
+                   (bf16_t *)X, (bf16_t *)X_lo, ssq);
+    else
+        kvr_launch(resid_gain_kernel<float>, grid, dim3(256), 0, s, H, part, nsplit, R, (const float *)gain, d,
+                   (bf16_t *)X, (bf16_t *)X_lo, ssq);
     return hipGetLastError();
 }
 
