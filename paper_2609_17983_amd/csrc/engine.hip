@@ -43,7 +43,8 @@ struct kvr_ctx {
 
     // projection weights repacked in operand order (bf16 MFMA paths)
     struct PackedLayer { const void *qkv, *o, *gu, *down; };
-    int gu_grp = 1;  // tile group of the packed gate/up weights (packed_tile_offset)
+    // tile group of each projection's packed weights (packed_tile_offset)
+    int qkv_grp = 1, o_grp = 1, gu_grp = 1, down_grp = 1;
     std::vector<PackedLayer> pk;
     char *wpk = nullptr;
     size_t wpk_bytes = 0;
@@ -418,7 +419,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     const bool bf = c->bf16;
     SkinnyPlan p_qkv{}, p_o{}, p_gu{}, p_down{};
     if (sk) {
-        p_qkv = plan_skinny(NQKV / 16, D, R, false, 16, "KVR_NT_QKV", "KVR_SPLIT_QKV");
+        p_qkv = plan_skinny(NQKV / 16, D, R, false, 8, "KVR_NT_QKV", "KVR_SPLIT_QKV");
         p_o = plan_skinny(D / 16, qd, R, false, 8, "KVR_NT_O", "KVR_SPLIT_O");
         p_gu = plan_skinny(2 * F / 16, D, R, true, 16, "KVR_NT_GATEUP", nullptr);
         p_down = plan_skinny(D / 16, F, R, false, 8, "KVR_NT_DOWN", "KVR_SPLIT_DOWN");
@@ -448,13 +449,14 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                       "rmsnorm(attn)", ST_NORM);
         int qkv_split = 1;
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, 1, c->P, nullptr, p_qkv, s, c->rs_ssq,
+            KVR_CHECK(skinny(EPI_STORE, c->Xn, c->Xn_lo, R, D, NQKV, pw.qkv, c->qkv_grp, c->P, nullptr, p_qkv, s, c->rs_ssq,
                              d.rms_eps),
                       "qkv", ST_QKV);
             qkv_split = p_qkv.split;
         } else {
             LinearArgs a = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr,
                                      NQKV);
+            a.grp = c->qkv_grp;
             if (pw.qkv) a.split = tiled_split(c, R, NQKV, D);
             KVR_CHECK(linear(c, EPI_STORE, a, s), "qkv", ST_QKV);
             qkv_split = a.split;
@@ -483,11 +485,12 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             if (l == d.n_layers - 1) return KVR_OK;
         }
         if (sk) {
-            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, 1, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
+            KVR_CHECK(skinny(EPI_STORE, c->Ob, c->Ob_lo, R, qd, D, pw.o, c->o_grp, c->P, nullptr, p_o, s), "o_proj", ST_OPROJ);
             resid_split = p_o.split;
         } else if (pw.o) {
             // packed: partial tiles into P (the next RMSNorm adds them to H)
             LinearArgs a = make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->P, nullptr, D);
+            a.grp = c->o_grp;
             a.split = tiled_split(c, R, D, qd);
             KVR_CHECK(linear(c, EPI_STORE, a, s), "o_proj", ST_OPROJ);
             resid_split = a.split;
@@ -507,7 +510,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             KVR_CHECK(skinny(EPI_SWIGLU, c->Xn, c->Xn_lo, R, D, F, pw.gu, c->gu_grp, c->Ab, c->Ab_lo, p_gu, s, c->rs_ssq,
                              d.rms_eps),
                       "gate_up", ST_GATEUP);
-            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, 1, c->P, nullptr, p_down, s), "down",
+            KVR_CHECK(skinny(EPI_STORE, c->Ab, c->Ab_lo, R, F, D, pw.down, c->down_grp, c->P, nullptr, p_down, s), "down",
                       ST_DOWN);
             resid_split = p_down.split;
         } else {
@@ -518,6 +521,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             if (pw.down) {
                 LinearArgs a = make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down, c->P,
                                          nullptr, D);
+                a.grp = c->down_grp;
                 a.split = tiled_split(c, R, D, F);
                 KVR_CHECK(linear(c, EPI_STORE, a, s), "down", ST_DOWN);
                 resid_split = a.split;
@@ -755,26 +759,30 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
         }
         c->pk.resize(d.n_layers);
         // gate/up tiles are stored in groups of the tile count a skinny block
-        // streams (the plan for a repair of up to 64 rows), so that each block
-        // reads one contiguous range; the other projections split K over
-        // blocks and gain nothing from it
-        c->gu_grp = plan_skinny(2 * F / 16, D, std::min(64, std::max(1, d.max_rows)), true, 16, nullptr, nullptr).nt;
+        // streams (the plan for a repair of up to 64 rows), so that a block
+        // reads one contiguous range: 8B shape, 48 rows, 47.8 -> 44.5 us.  The
+        // tiled kernel pays 2-4 % for grouped weights (Qwen shape at 528 rows,
+        // batched repair); for the other projections, which split K over
+        // blocks, grouping gained the skinny path under 1 % and they stay
+        // tile-major.
+        const int rref = std::min(64, std::max(1, d.max_rows));
+        c->gu_grp = plan_skinny(2 * F / 16, D, rref, true, 16, nullptr, nullptr).nt;
         bf16_t *dst = (bf16_t *)c->wpk;
         for (int l = 0; l < d.n_layers && e == hipSuccess; ++l) {
             const kvr_layer_weights &w = c->layers[l];
             kvr_ctx::PackedLayer &pl = c->pk[l];
             pl.qkv = dst;
-            e = launch_pack_weight(w.wq, w.wk, w.wv, qd, qd + kd, false, NQKV, D, 1, dst, 0);
+            e = launch_pack_weight(w.wq, w.wk, w.wv, qd, qd + kd, false, NQKV, D, c->qkv_grp, dst, 0);
             dst += (size_t)NQKV * D;
             pl.o = dst;
-            if (e == hipSuccess) e = launch_pack_weight(w.wo, w.wo, w.wo, D, D, false, D, qd, 1, dst, 0);
+            if (e == hipSuccess) e = launch_pack_weight(w.wo, w.wo, w.wo, D, D, false, D, qd, c->o_grp, dst, 0);
             dst += (size_t)D * qd;
             pl.gu = dst;
             if (e == hipSuccess)
                 e = launch_pack_weight(w.w_gate, w.w_up, w.w_up, F, 2 * F, true, 2 * F, D, c->gu_grp, dst, 0);
             dst += (size_t)2 * F * D;
             pl.down = dst;
-            if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, 1, dst, 0);
+            if (e == hipSuccess) e = launch_pack_weight(w.w_down, w.w_down, w.w_down, D, D, false, D, F, c->down_grp, dst, 0);
             dst += (size_t)D * F;
         }
         if (e == hipSuccess && d.vocab % 16 == 0) {

@@ -122,11 +122,17 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
             src[i] = (const bf16_t *)a.wp + packed_tile_offset(t, ntiles, ksteps, a.grp, &kstride[i]) + lane * 8;
         }
     }
+    // k-steps are issued in order, so each fragment keeps a running pointer
+    // (one add per k-step, no multiply by the stride in the loop)
+#pragma unroll
+    for (int i = 0; i < FPW; ++i) src[i] += (size_t)k0 * kstride[i];
     auto issue = [&](int kk) {
         bf16_t *st = lds + (kk % STAGES) * STAGE + FPW * w * FRAG;
 #pragma unroll
-        for (int i = 0; i < FPW; ++i)
-            __builtin_amdgcn_global_load_lds(src[i] + (size_t)(k0 + kk) * kstride[i], st + i * FRAG, 16, 0, 0);
+        for (int i = 0; i < FPW; ++i) {
+            __builtin_amdgcn_global_load_lds(src[i], st + i * FRAG, 16, 0, 0);
+            src[i] += kstride[i];
+        }
     };
 
     f32x4 acc[4][JT];
