@@ -337,35 +337,41 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
     }
 }
 
-// One block per (combine item, query head of the group, row), one thread per
-// head dimension: merge the split partials of one row with log-sum-exp
-// weights (exp2 domain), summing the parts in ascending order.  With at most
-// NP parts every partial of the row is loaded in one round (clamped indexes,
-// so the loads are unconditional and all in flight together); longer lists
-// take batches of NP.  `lse` as above.
+// One wavefront per (combine item, query head of the group, two rows): each
+// half-wavefront takes one row, a lane four consecutive head dimensions.  The
+// split partials of the row are merged with log-sum-exp weights (exp2
+// domain), the parts summed in ascending order.  With at most NP parts every
+// partial of the row is loaded in one round (clamped indexes, so the loads
+// are unconditional and all in flight together); longer lists take batches
+// of NP.  `lse` as above.
 template <int NP>
-__global__ __launch_bounds__(128) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
-                                                                int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm,
-                                                                float *lse) {
+__global__ __launch_bounds__(64) void attention_combine_kernel(const CombineItem *items, const float *part, int Hq,
+                                                               int Hkv, int MT, bf16_t *O, bf16_t *O_lo, int o_perm,
+                                                               float *lse) {
+    static_assert(HD == 128, "a half-wavefront covers one head row");
     const CombineItem it = items[blockIdx.x];
-    const int t = blockIdx.y, i = blockIdx.z;
+    const int t = blockIdx.y;
+    const int lane = threadIdx.x;
+    const int i = 2 * blockIdx.z + (lane >> 5);
     if (i >= it.nrows) return;
     const int G = Hq / Hkv;
     const int rows_item = 16 * MT;
     const int j = it.kvh * G + t;
-    const int d = threadIdx.x;  // 0..127
+    const int d = 4 * (lane & 31);
     const size_t qstride = (size_t)G * rows_item * PART_ROW;
     const float *base = part + ((size_t)(it.part0 * G + t) * rows_item + i) * PART_ROW;
     const int np = it.nparts;
-    float M = -INFINITY, acc = 0.f, L = 0.f;
+    float M = -INFINITY, L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int q0 = 0; q0 < np; q0 += NP) {
-        float mm[NP], ll[NP], oo[NP];
+        float mm[NP], ll[NP];
+        f32x4 oo[NP];
 #pragma unroll
         for (int u = 0; u < NP; ++u) {
             const float *p = base + (size_t)min(q0 + u, np - 1) * qstride;
             mm[u] = p[HD];
             ll[u] = p[HD + 1];
-            oo[u] = p[d];
+            oo[u] = *reinterpret_cast<const f32x4 *>(p + d);
         }
         float Mb = M;
 #pragma unroll
@@ -381,8 +387,19 @@ __global__ __launch_bounds__(128) void attention_combine_kernel(const CombineIte
         }
         M = Mb;
     }
-    const int r = it.row0 + i, c = j * HD + d;
-    store_operand(O, O_lo, o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c, acc / L);
+    const int r = it.row0 + i, c = j * HD + d;  // four consecutive columns (adjacent in operand order too)
+    const size_t off = o_perm ? perm_offset(r, c, Hq * HD) : (size_t)r * Hq * HD + c;
+    const f32x4 y = acc / L;
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const bf16_t h0 = f32_to_bf16(y[2 * q]), h1 = f32_to_bf16(y[2 * q + 1]);
+        const bf16_t l0 = f32_to_bf16(y[2 * q] - bf16_to_f32(h0)), l1 = f32_to_bf16(y[2 * q + 1] - bf16_to_f32(h1));
+        hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    }
+    *reinterpret_cast<uint2 *>(O + off) = make_uint2(hi[0], hi[1]);
+    *reinterpret_cast<uint2 *>(O_lo + off) = make_uint2(lo[0], lo[1]);
     if (lse && d == 0) lse[(size_t)r * Hq + j] = M + log2f(L);
 }
 
@@ -419,7 +436,7 @@ hipError_t launch_attention_combine(const CombineItem *items, int n_items, int M
                                     int Hkv, bf16_t *O, bf16_t *O_lo, bool o_perm, float *lse, hipStream_t s) {
     if (n_items <= 0) return hipSuccess;
     if (MT < 1 || MT > attention_max_row_tiles(Hq, Hkv)) return hipErrorInvalidValue;
-    kvr_launch(attention_combine_kernel<COMBINE_NP>, dim3(n_items, Hq / Hkv, 16 * MT), dim3(128), 0, s, items, part,
+    kvr_launch(attention_combine_kernel<COMBINE_NP>, dim3(n_items, Hq / Hkv, 8 * MT), dim3(64), 0, s, items, part,
                Hq, Hkv, MT, O, O_lo, (int)o_perm, lse);
     return hipGetLastError();
 }
