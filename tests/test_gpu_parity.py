@@ -360,3 +360,37 @@ def test_wide_repair_split_tiled_projections():
         _repair_case(shape, eng, ow, stale, new, 200, 216, A, f"{shape.name} EditLocal K=150 (166 rows)")
     finally:
         eng.close()
+
+
+# 4160 features: 520 gate/up weight tiles, which the engine packs in groups of
+# three (the skinny plan's tiles per block for up to 64 rows), so the last
+# group holds a single tile.  Prefill reads the grouped weights through the
+# tiled kernel, the 48-row repair through the skinny kernel.
+RAGGED = synth.ModelShape("ragged-groups-bf16", 1, 512, 8, 2, 128, 4160, 2048, 1e-5, 500000.0)
+
+
+def test_ragged_gateup_groups_prefill_and_repair():
+    shape, n = RAGGED, 700
+    w = synth.make_weights(shape, dtype=torch.bfloat16, seed=9)
+    eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=64)
+    try:
+        toks = synth.make_tokens(n, shape.vocab, seed=10)
+        cache = eng.new_cache(n)
+        hidden = torch.empty((n, shape.d_model), device="cuda")
+        say(f"case: {shape.name} prefill n={n}")
+        eng.prefill(toks.cuda(), cache, hidden)
+        torch.cuda.synchronize()
+        oc, oy = od.prefill(shape, OracleWeights(w), toks.numpy())
+        got = cache.to(torch.float64).cpu().numpy()
+        errs = {(l, kv): relmax(got[l, kv], oc[l, kv]) for l in range(shape.n_layers) for kv in range(2)}
+        errs["hidden"] = relmax(hidden.cpu().numpy(), oy)
+        say(f"  {errs}")
+        assert max(errs.values()) <= TOL[kvr.KVR_BF16]
+
+        ow = OracleWeights(w, cache=True)
+        stale = synth.make_stale_cache(shape, n, label=9).to(torch.float64).numpy()
+        new = synth.apply_edit(toks, 300, 16, shape.vocab)
+        A = osel.select_edit_local(n, 300, 316, 32)
+        _repair_case(shape, eng, ow, stale, new, 300, 316, A, f"{shape.name} EditLocal K=32 (48 rows)")
+    finally:
+        eng.close()
