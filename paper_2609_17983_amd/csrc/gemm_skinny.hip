@@ -18,12 +18,17 @@
 // with the k-step D further on, so the memory pipe never drains between
 // batches.
 //
+// The tiles may be stored in groups (packed_tile_offset): when a block's NT
+// tiles form one group, its weight stream is one contiguous range.
+//
 // Blocks never exchange data: with split > 1 each block writes an fp32 partial
 // tile [split][R][N] and the row-wise kernel that runs next sums the partials
 // in a fixed order (deterministic, and free of device-wide fences).  The
 // gate/up projection is never split; its weight is gate/up interleaved (tile t
 // = gate rows 8t..8t+7, then up rows 8t..8t+7) and the epilogue applies
-// SwiGLU, writing the down projection's operand.
+// SwiGLU, writing the down projection's operand.  When X is an unnormalised
+// H * gain (skinny passes, resid_gain), the epilogue multiplies each output
+// row by its RMSNorm scale first.
 #include "common.h"
 
 namespace kvr {
