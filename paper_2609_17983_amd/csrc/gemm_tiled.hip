@@ -35,6 +35,8 @@
 // XCD x runs range x in order: the blocks an XCD runs together cover about
 // four row blocks by eight column blocks, whose activation and weight slabs
 // its L2 shares.
+#include <stdlib.h>
+
 #include <algorithm>
 
 #include "common.h"
@@ -44,23 +46,28 @@ namespace kvr {
 namespace {
 
 constexpr int WT = 16;          // 16-row weight tiles per block (256 output columns)
-constexpr int STAGES = 2;       // k-steps held in the LDS ring
 constexpr int FRAG = 512;       // bf16 elements of one 16 x 32 operand fragment
 constexpr int XCDS = 8;         // L2 domains the workgroups are dealt to in turn
 constexpr int GROUP_M = 4;      // row blocks per group of the tile order
 
-// Block shape for RT 16-row activation tiles (8: 128 rows, two blocks per
-// compute unit; 4: 64 rows, three blocks per unit, for grids that would
-// otherwise not fill the chip): wavefronts in WM rows x WN columns, each
-// owning 4 row tiles x JT weight tiles.
+// Block shape for RT 16-row activation tiles: wavefronts in WM rows x WN
+// columns, each owning 4 row tiles x JT weight tiles (64 x 128 or 64 x 64).
+//   RT = 16: 256 rows, eight wavefronts, three LDS stages (144 KB), one block
+//            per compute unit: the weight tile of a k-step serves 256 rows;
+//   RT = 8:  128 rows, four wavefronts, two stages, two blocks per unit;
+//   RT = 4:  64 rows, four wavefronts, two stages, three blocks per unit, for
+//            grids that would otherwise not fill the chip.
 template <int RT>
 struct TileShape {
-    static constexpr int NFRAG = 2 * RT + WT;  // fragments per k-step: X hi, X lo, W
+    static constexpr int NW = RT == 16 ? 8 : 4;      // wavefronts per block
+    static constexpr int STAGES = RT == 16 ? 3 : 2;  // k-steps held in the LDS ring
+    static constexpr int NFRAG = 2 * RT + WT;        // fragments per k-step: X hi, X lo, W
     static constexpr int STAGE = NFRAG * FRAG;
-    static constexpr int FPW = NFRAG / 4;      // fragments each wavefront loads per k-step
-    static constexpr int WM = RT / 4, WN = 4 / WM, JT = WT / WN;
-    static constexpr int BLOCKS_PER_CU = RT == 8 ? 2 : 3;
-    static_assert(NFRAG % 4 == 0 && WM * WN == 4, "four wavefronts per block");
+    static constexpr int FPW = NFRAG / NW;           // fragments each wavefront loads per k-step
+    static constexpr int WM = RT / 4, WN = NW / WM, JT = WT / WN;
+    static constexpr int BLOCKS_PER_CU = RT == 16 ? 1 : (RT == 8 ? 2 : 3);
+    static_assert(NFRAG % NW == 0 && WM * WN == NW && FPW <= 8, "block shape");
+    static_assert(STAGES * STAGE * 2 <= 160 * 1024, "LDS");
 };
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
@@ -77,10 +84,19 @@ __device__ __forceinline__ void lds_barrier() {
 // (expcnt and lgkmcnt left unconstrained).
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x70 | 0xF00); }
 
+// Wait until at most n of this wavefront's vector-memory loads are in flight
+// (n a compile-time count below 16).
+template <int N>
+__device__ __forceinline__ void wait_loads_upto() {
+    static_assert(N >= 0 && N < 16, "vmcnt immediate");
+    __builtin_amdgcn_s_waitcnt(0x70 | 0xF00 | N);
+}
+
 template <int EPI, int RT>
-__global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tiled_kernel(LinearArgs a) {
+__global__ __launch_bounds__(64 * TileShape<RT>::NW, TileShape<RT>::BLOCKS_PER_CU) void linear_tiled_kernel(
+    LinearArgs a) {
     using S = TileShape<RT>;
-    constexpr int STAGE = S::STAGE, FPW = S::FPW, JT = S::JT;
+    constexpr int STAGE = S::STAGE, FPW = S::FPW, JT = S::JT, STAGES = S::STAGES;
     __shared__ __attribute__((aligned(16))) bf16_t lds[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -145,7 +161,10 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < nk) issue(s);
     for (int kk = 0; kk < nk; ++kk) {
-        wait_loads();   // this wavefront's loads of k-step kk (the only ones in flight)
+        // this wavefront's loads of k-step kk have landed (with three stages
+        // the loads of kk + 1, issued later, may still be in flight)
+        if (STAGES == 3 && kk + 1 < nk) wait_loads_upto<(STAGES == 3 ? FPW : 0)>();
+        else wait_loads();
         lds_barrier();  // every wavefront's loads of kk have landed; all reads of kk - 1 are done
         if (kk + STAGES - 1 < nk) issue(kk + STAGES - 1);  // into the slot k-step kk - 1 used
 
@@ -215,20 +234,41 @@ __global__ __launch_bounds__(256, TileShape<RT>::BLOCKS_PER_CU) void linear_tile
 template <int RT>
 void launch_rt(int epi, const LinearArgs &a, int tiles, hipStream_t s) {
     dim3 grid((tiles + XCDS - 1) / XCDS * XCDS, epi == EPI_STORE ? std::max(1, (int)a.split) : 1);
-    if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE, RT>, grid, dim3(256), 0, s, a);
-    else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID, RT>, grid, dim3(256), 0, s, a);
-    else kvr_launch(linear_tiled_kernel<EPI_SWIGLU, RT>, grid, dim3(256), 0, s, a);
+    const dim3 block(64 * TileShape<RT>::NW);
+    if (epi == EPI_STORE) kvr_launch(linear_tiled_kernel<EPI_STORE, RT>, grid, block, 0, s, a);
+    else if (epi == EPI_RESID) kvr_launch(linear_tiled_kernel<EPI_RESID, RT>, grid, block, 0, s, a);
+    else kvr_launch(linear_tiled_kernel<EPI_SWIGLU, RT>, grid, block, 0, s, a);
+}
+
+// Row tiles per block for R rows and vrows weight rows.  256-row blocks
+// (one per compute unit) only when they make at least eight rounds: their
+// last, partial round costs a whole one (8B gate/up at 5000 rows, 8.75
+// rounds: prefill 132.1 -> 128.1 ms; at 3072 rows, 5.25 rounds: 33.0 ->
+// 37.2 ms).  Else 128-row blocks when there is one per unit (a K split then
+// brings them to two per unit: batched down 17.5 -> 15.8 ms against 64-row
+// blocks), else 64-row blocks.  A larger block is taken only if it pads at
+// most 5 % more row tiles than the next smaller one (144 rows are 9 row
+// tiles: 16 in 128-row blocks against 12 in 64-row ones; Qwen gate/up 4.5
+// against 3.0 ms).  KVR_TILED_RT (4, 8, 16) forces a shape.
+static int tiled_rt(int R, int vrows) {
+    const int rtiles = (R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
+    if (const char *e = getenv("KVR_TILED_RT")) {
+        const int v = atoi(e);
+        if (v == 4 || v == 8 || v == 16) return v;
+    }
+    auto padded = [&](int rt) { return (rtiles + rt - 1) / rt * rt; };
+    const bool fits8 = 20 * padded(8) <= 21 * padded(4), fits16 = 20 * padded(16) <= 21 * padded(8);
+    if (fits8 && fits16 && (rtiles + 15) / 16 * nb >= 8 * 256) return 16;
+    if (fits8 && (rtiles + 7) / 8 * nb >= 256) return 8;
+    return 4;
 }
 
 int tiled_blocks(int R, int vrows, int *slots) {
     const int rtiles = (R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
-    const int tiles8 = (rtiles + 7) / 8 * nb;
-    if (tiles8 >= TileShape<8>::BLOCKS_PER_CU * 256) {
-        if (slots) *slots = TileShape<8>::BLOCKS_PER_CU * 256;
-        return tiles8;
-    }
-    if (slots) *slots = TileShape<4>::BLOCKS_PER_CU * 256;
-    return (rtiles + 3) / 4 * nb;
+    const int rt = tiled_rt(R, vrows);
+    if (slots) *slots = (rt == 16 ? TileShape<16>::BLOCKS_PER_CU : rt == 8 ? TileShape<8>::BLOCKS_PER_CU
+                                                                           : TileShape<4>::BLOCKS_PER_CU) * 256;
+    return (rtiles + rt - 1) / rt * nb;
 }
 
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
@@ -237,12 +277,11 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     if (a.K % 32 != 0 || vrows % 16 != 0) return hipErrorInvalidValue;
     if (a.split > 1 && (epi != EPI_STORE || a.split > a.K / 32)) return hipErrorInvalidValue;
-    const int rtiles = (a.R + 15) / 16, nb = (vrows / 16 + WT - 1) / WT;
-    // 128-row blocks unless they would not give every compute unit its two
-    // blocks; then 64-row blocks, three per unit
-    const int tiles8 = (rtiles + 7) / 8 * nb;
-    if (tiles8 >= TileShape<8>::BLOCKS_PER_CU * 256) launch_rt<8>(epi, a, tiles8, s);
-    else launch_rt<4>(epi, a, (rtiles + 3) / 4 * nb, s);
+    const int rt = tiled_rt(a.R, vrows);
+    const int blocks = tiled_blocks(a.R, vrows, nullptr);
+    if (rt == 16) launch_rt<16>(epi, a, blocks, s);
+    else if (rt == 8) launch_rt<8>(epi, a, blocks, s);
+    else launch_rt<4>(epi, a, blocks, s);
     return hipGetLastError();
 }
 

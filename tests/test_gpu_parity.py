@@ -394,3 +394,29 @@ def test_ragged_gateup_groups_prefill_and_repair():
         _repair_case(shape, eng, ow, stale, new, 300, 316, A, f"{shape.name} EditLocal K=32 (48 rows)")
     finally:
         eng.close()
+
+
+def test_wide_prefill_256_row_blocks(monkeypatch):
+    """The tiled kernel's 256-row shape (eight wavefronts, three LDS stages),
+    which the launcher picks only for grids of eight rounds or more, forced
+    on the 1100-row prefill: five row blocks, the last one holding 5 of its 16
+    row tiles."""
+    monkeypatch.setenv("KVR_TILED_RT", "16")
+    shape, n = WIDE, 1100
+    w = synth.make_weights(shape, dtype=torch.bfloat16, seed=11)
+    eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=64)
+    try:
+        toks = synth.make_tokens(n, shape.vocab, seed=12)
+        cache = eng.new_cache(n)
+        hidden = torch.empty((n, shape.d_model), device="cuda")
+        say(f"case: {shape.name} prefill n={n}, 256-row tiles")
+        eng.prefill(toks.cuda(), cache, hidden)
+        torch.cuda.synchronize()
+        oc, oy = od.prefill(shape, OracleWeights(w), toks.numpy())
+        got = cache.to(torch.float64).cpu().numpy()
+        errs = {(l, kv): relmax(got[l, kv], oc[l, kv]) for l in range(shape.n_layers) for kv in range(2)}
+        errs["hidden"] = relmax(hidden.cpu().numpy(), oy)
+        say(f"  {errs}")
+        assert max(errs.values()) <= TOL[kvr.KVR_BF16]
+    finally:
+        eng.close()
