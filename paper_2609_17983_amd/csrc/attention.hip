@@ -60,14 +60,26 @@ typedef __attribute__((ext_vector_type(2))) float f32x2;
 
 __device__ __forceinline__ bf16x8 ld16(const bf16_t *p) { return *reinterpret_cast<const bf16x8 *>(p); }
 
-// reductions over the four lanes l, l^16, l^32, l^48 that hold one query row
+// Reductions over the four lanes l, l^16, l^32, l^48 that hold one query row.
+// v_permlane16_swap (v_permlane32_swap) run with both operands equal to v hand
+// every lane the pair {v[l], v[l^16]} ({v[l], v[l^32]}), in an order that is the
+// same for both lanes of the pair, so one VALU op per step completes each
+// butterfly without an LDS round trip and all four lanes end bit-identical.
 __device__ __forceinline__ float xmax4(float v) {
-    v = fmaxf(v, __shfl_xor(v, 16, 64));
-    return fmaxf(v, __shfl_xor(v, 32, 64));
+    unsigned u = __float_as_uint(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    u = __float_as_uint(v);
+    const auto b = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float xsum4(float v) {
-    v += __shfl_xor(v, 16, 64);
-    return v + __shfl_xor(v, 32, 64);
+    unsigned u = __float_as_uint(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    u = __float_as_uint(v);
+    const auto b = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // PPW: (head, row tile) pairs per wavefront; MT: row tiles of a full item.
