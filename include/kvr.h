@@ -65,6 +65,9 @@ typedef enum { KVR_F32 = 0, KVR_BF16 = 1 } kvr_dtype;
 
 /* Model and workspace dimensions.
  * head_dim must be even and at most 128; n_heads a multiple of n_kv_heads.
+ * d_model must be a multiple of 4 and at most 16384, and the fused
+ * projection width (n_heads + 2 n_kv_heads) * head_dim a multiple of 4;
+ * other shapes give KVR_E_UNSUPPORTED.
  * max_ctx bounds n_cap of every cache the context is used with (it sizes the
  * rotary table); max_rows bounds the total number of repaired rows |P| summed
  * over the documents of one kvr_repair call.  fp32 computes every step in

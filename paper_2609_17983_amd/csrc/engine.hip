@@ -619,6 +619,10 @@ kvr_status check_dims(const kvr_dims *d) {
     if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.0)) return KVR_E_ARG;
     if (d->dtype != KVR_F32 && d->dtype != KVR_BF16) return KVR_E_ARG;
     if (d->head_dim > 128) return KVR_E_UNSUPPORTED;
+    // the row kernels move four floats per access over d_model (at most 16384)
+    // and over the fused Q|K|V row of (n_heads + 2 n_kv_heads) head_dim values
+    if (d->d_model % 4 != 0 || d->d_model > 16384 || ((d->n_heads + 2 * d->n_kv_heads) * d->head_dim) % 4 != 0)
+        return KVR_E_UNSUPPORTED;
     return KVR_OK;
 }
 

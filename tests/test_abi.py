@@ -88,6 +88,13 @@ def test_cache_bytes():
     assert kvr.kvr_cache_bytes(_dims(), 512) == 2 * 2 * 4 * 512 * 64 * 4
     assert kvr.kvr_cache_bytes(_dims(dtype=kvr.KVR_BF16, n_kv_heads=2), 100) == 2 * 2 * 2 * 100 * 64 * 2
     assert kvr.kvr_cache_bytes(_dims(n_heads=3, n_kv_heads=2), 10) == 0
+    # shapes the row kernels cannot take are rejected when the dims are
+    # checked, before any launch: d_model not a multiple of 4 or above 16384,
+    # fused Q|K|V width (3 + 2) * 6 = 30 not a multiple of 4
+    assert kvr.kvr_cache_bytes(_dims(d_model=250), 10) == 0
+    assert kvr.kvr_cache_bytes(_dims(d_model=16388), 10) == 0
+    assert kvr.kvr_cache_bytes(_dims(d_model=24, n_heads=3, n_kv_heads=1, head_dim=6), 10) == 0
+    assert kvr.kvr_cache_bytes(_dims(d_model=24, n_heads=4, n_kv_heads=2, head_dim=6), 10) == 2 * 2 * 2 * 10 * 6 * 4
 
 
 @pytest.mark.parametrize("bad,status", [

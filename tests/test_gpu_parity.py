@@ -396,6 +396,52 @@ def test_ragged_gateup_groups_prefill_and_repair():
         eng.close()
 
 
+# head_dim 12 (even, not a multiple of 8) and d_model 48: RoPE and the cache
+# scatter take the row kernel that stages the fused Q|K|V row in LDS, and the
+# projections and attention the generic kernels (the MFMA paths need 64-wide
+# shapes and head_dim 128).
+ODD_HD = synth.ModelShape("odd-head-dim", 2, 48, 4, 2, 12, 80, 256, 1e-5, 10000.0)
+
+
+def _prefill_then_repair(shape, dtype, n, seed, edit, tag):
+    tdt = torch.bfloat16 if dtype == kvr.KVR_BF16 else torch.float32
+    w = synth.make_weights(shape, dtype=tdt, seed=seed)
+    eng = Engine(shape, to_device_weights(w), dtype, max_ctx=n, max_rows=64)
+    try:
+        toks = synth.make_tokens(n, shape.vocab, seed=seed + 1)
+        cache = eng.new_cache(n)
+        hidden = torch.empty((n, shape.d_model), device="cuda")
+        say(f"case: {tag} prefill n={n}")
+        eng.prefill(toks.cuda(), cache, hidden)
+        torch.cuda.synchronize()
+        ow = OracleWeights(w, cache=True)
+        oc, oy = od.prefill(shape, ow, toks.numpy())
+        got = cache.to(torch.float64).cpu().numpy()
+        errs = {(l, kv): relmax(got[l, kv], oc[l, kv]) for l in range(shape.n_layers) for kv in range(2)}
+        errs["hidden"] = relmax(hidden.cpu().numpy(), oy)
+        say(f"  {errs}")
+        assert max(errs.values()) <= TOL[dtype]
+        s0, s1 = edit
+        new = synth.apply_edit(toks, s0, s1 - s0, shape.vocab)
+        A = osel.select_edit_local(n, s0, s1, 32)
+        _repair_case(shape, eng, ow, oc, new, s0, s1, A, f"{tag} EditLocal K=32")
+    finally:
+        eng.close()
+
+
+@pytest.mark.parametrize("dtype", [kvr.KVR_F32, kvr.KVR_BF16], ids=["f32", "bf16"])
+def test_odd_head_dim_prefill_and_repair(dtype):
+    _prefill_then_repair(ODD_HD, dtype, 200, 13, (60, 68), f"{ODD_HD.name} {'bf16' if dtype else 'f32'}")
+
+
+def test_bf16_generic_kernels_forced(monkeypatch):
+    """KVR_SIMPLE=1 at context creation switches a bf16 model that the MFMA
+    kernels would take to the generic projection and attention kernels (the
+    reference path for debugging); it must meet the same bound."""
+    monkeypatch.setenv("KVR_SIMPLE", "1")
+    _prefill_then_repair(MID, kvr.KVR_BF16, 300, 15, (100, 116), "mid-bf16 generic kernels")
+
+
 def test_wide_prefill_256_row_blocks(monkeypatch):
     """The tiled kernel's 256-row shape (eight wavefronts, three LDS stages),
     which the launcher picks only for grids of eight rounds or more, forced
