@@ -396,6 +396,48 @@ def test_ragged_gateup_groups_prefill_and_repair():
         eng.close()
 
 
+# Skinny-GEMM plans forced through the planner's overrides (read on every
+# pass), so that every tile count per block (1-8), cross-block splits up to 8
+# and gate/up blocks whose tiles straddle the packing groups are checked
+# against the oracle, not only the plans the cost model picks.
+PLAN_OVERRIDES = [
+    {"KVR_NT_QKV": "1", "KVR_SPLIT_QKV": "1", "KVR_NT_O": "2", "KVR_SPLIT_O": "8", "KVR_NT_GATEUP": "1",
+     "KVR_NT_DOWN": "3", "KVR_SPLIT_DOWN": "2"},
+    {"KVR_NT_QKV": "5", "KVR_SPLIT_QKV": "2", "KVR_NT_O": "6", "KVR_SPLIT_O": "1", "KVR_NT_GATEUP": "4",
+     "KVR_NT_DOWN": "7", "KVR_SPLIT_DOWN": "4"},
+    {"KVR_NT_QKV": "8", "KVR_SPLIT_QKV": "4", "KVR_NT_O": "8", "KVR_SPLIT_O": "2", "KVR_NT_GATEUP": "6",
+     "KVR_NT_DOWN": "8", "KVR_SPLIT_DOWN": "8"},
+]
+
+
+@pytest.mark.parametrize("env", PLAN_OVERRIDES, ids=["nt1-2-3", "nt4-5-6-7", "nt6-8"])
+def test_mid_skinny_plan_overrides(mid, monkeypatch, env):
+    shape, eng, ow, toks, new, stale_np = mid
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    A = osel.select_edit_local(700, 300, 316, 32)
+    _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid EditLocal K=32, skinny plans {env}")
+
+
+@pytest.mark.parametrize("nt", ["2", "5"])
+def test_ragged_gateup_blocks_across_groups(monkeypatch, nt):
+    """Gate/up packed in groups of three tiles, read by blocks of two or five
+    tiles: every block's tiles start inside a group or straddle two."""
+    monkeypatch.setenv("KVR_NT_GATEUP", nt)
+    shape, n = RAGGED, 700
+    w = synth.make_weights(shape, dtype=torch.bfloat16, seed=9)
+    eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=64)
+    try:
+        toks = synth.make_tokens(n, shape.vocab, seed=10)
+        ow = OracleWeights(w, cache=True)
+        stale = synth.make_stale_cache(shape, n, label=9).to(torch.float64).numpy()
+        new = synth.apply_edit(toks, 300, 16, shape.vocab)
+        A = osel.select_edit_local(n, 300, 316, 32)
+        _repair_case(shape, eng, ow, stale, new, 300, 316, A, f"{shape.name} gate/up blocks of {nt} tiles")
+    finally:
+        eng.close()
+
+
 # head_dim 12 (even, not a multiple of 8) and d_model 48: RoPE and the cache
 # scatter take the row kernel that stages the fused Q|K|V row in LDS, and the
 # projections and attention the generic kernels (the MFMA paths need 64-wide
