@@ -484,12 +484,14 @@ def test_bf16_generic_kernels_forced(monkeypatch):
     _prefill_then_repair(MID, kvr.KVR_BF16, 300, 15, (100, 116), "mid-bf16 generic kernels")
 
 
-def test_wide_prefill_256_row_blocks(monkeypatch):
-    """The tiled kernel's 256-row shape (eight wavefronts, three LDS stages),
-    which the launcher picks only for grids of eight rounds or more, forced
-    on the 1100-row prefill: five row blocks, the last one holding 5 of its 16
-    row tiles."""
-    monkeypatch.setenv("KVR_TILED_RT", "16")
+@pytest.mark.parametrize("rt", ["16", "8", "4"])
+def test_wide_prefill_forced_row_blocks(monkeypatch, rt):
+    """Each of the tiled kernel's row-block shapes forced on the 1100-row
+    prefill (69 row tiles of 16): 256 rows (eight wavefronts, three LDS
+    stages; the launcher picks it only for grids of eight rounds or more),
+    128 rows (two stages, two blocks per compute unit) and 64 rows; the last
+    row block is partial in each."""
+    monkeypatch.setenv("KVR_TILED_RT", rt)
     shape, n = WIDE, 1100
     w = synth.make_weights(shape, dtype=torch.bfloat16, seed=11)
     eng = Engine(shape, to_device_weights(w), kvr.KVR_BF16, max_ctx=n, max_rows=64)
@@ -497,7 +499,7 @@ def test_wide_prefill_256_row_blocks(monkeypatch):
         toks = synth.make_tokens(n, shape.vocab, seed=12)
         cache = eng.new_cache(n)
         hidden = torch.empty((n, shape.d_model), device="cuda")
-        say(f"case: {shape.name} prefill n={n}, 256-row tiles")
+        say(f"case: {shape.name} prefill n={n}, {16 * int(rt)}-row blocks")
         eng.prefill(toks.cuda(), cache, hidden)
         torch.cuda.synchronize()
         oc, oy = od.prefill(shape, OracleWeights(w), toks.numpy())
