@@ -419,6 +419,22 @@ def test_mid_skinny_plan_overrides(mid, monkeypatch, env):
     _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid EditLocal K=32, skinny plans {env}")
 
 
+# Attention plans forced through the planner's overrides: items of two or
+# three row tiles when keys are split (the combine then merges multi-tile
+# items), one-tile key ranges, and a target so low that no key range is split.
+ATT_OVERRIDES = [{"KVR_ATT_MT": "2"}, {"KVR_ATT_MT": "3"}, {"KVR_ATT_MINKS": "64", "KVR_ATT_TARGET": "1024"},
+                 {"KVR_ATT_TARGET": "1"}]
+
+
+@pytest.mark.parametrize("env", ATT_OVERRIDES, ids=["mt2", "mt3", "one-tile-items", "unsplit"])
+def test_mid_attention_plan_overrides(mid, monkeypatch, env):
+    shape, eng, ow, toks, new, stale_np = mid
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    A = osel.select_edit_local(700, 300, 316, 32)
+    _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid EditLocal K=32, attention plan {env}")
+
+
 @pytest.mark.parametrize("nt", ["2", "5"])
 def test_ragged_gateup_blocks_across_groups(monkeypatch, nt):
     """Gate/up packed in groups of three tiles, read by blocks of two or five
