@@ -53,6 +53,16 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     __shared__ __attribute__((aligned(16))) float red[4][MT * 16 * (FW + 4)];  // each wavefront's partial sums
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    // RMS row scale (see SkinnyArgs): the first four sums of squares of this
+    // thread's row are loaded now, ahead of every weight load, so that they
+    // have arrived when the epilogue adds them (R <= 16 MT, so these threads
+    // hold rows of the output)
+    const bool rs_row = a.rs_ssq && (int)threadIdx.x < a.R;
+    float rs_pre[4] = {0.f, 0.f, 0.f, 0.f};
+    if (rs_row) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) rs_pre[q] = a.rs_ssq[(size_t)min(q, a.rs_nb - 1) * a.R + threadIdx.x];
+    }
     const int split = a.split;
     const int tg = blockIdx.x / split, sp = blockIdx.x - tg * split;
     const int ksteps = a.K >> 5;
@@ -151,9 +161,12 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
     __shared__ float rscale[MT * 16];
     if (threadIdx.x < MT * 16) {
         float sc = 1.f;
-        if (a.rs_ssq && (int)threadIdx.x < a.R) {
-            float t = 0.f;
-            for (int b = 0; b < a.rs_nb; ++b) t += a.rs_ssq[(size_t)b * a.R + threadIdx.x];
+        if (rs_row) {
+            float t = 0.f;  // the sums in slice order
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (q < a.rs_nb) t += rs_pre[q];
+            for (int b = 4; b < a.rs_nb; ++b) t += a.rs_ssq[(size_t)b * a.R + threadIdx.x];
             sc = rsqrtf(t / (float)a.rs_d + a.rs_eps);
         }
         rscale[threadIdx.x] = sc;
