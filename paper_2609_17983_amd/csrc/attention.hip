@@ -43,7 +43,10 @@ constexpr int HD = ATT_HD;
 constexpr int KT = ATT_KT;
 constexpr int WAVES = 8;           // wavefronts per block
 constexpr int NLD = 16 / WAVES;    // 16-byte K (and V) loads per thread per tile
-constexpr int KS_STRIDE = HD + 8;  // key and value tile row stride (bf16)
+constexpr int KS_STRIDE = HD + 8;   // key tile row stride (bf16): rows 4 banks apart, so the 16
+                                    // rows of a key fragment read fall on distinct banks
+constexpr int VS_STRIDE = HD + 16;  // value tile row stride: rows 8 banks apart, so the four rows
+                                    // a transposing read takes per 16 lanes fall on distinct banks
 constexpr int PART_ROW = HD + 4;   // floats per (head, row) partial: O[128], m, l
 constexpr float RESCALE_SLACK = 8.0f;  // log2 headroom before the running max is raised
 constexpr int COMBINE_NP = 16;         // partials per row loaded in one round by the combine
@@ -91,7 +94,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                                                                     int o_perm, float *lse) {
     // KG 64-key K tiles, then KG V tiles (one per key group); after the key
     // loop the same memory takes the second key group's softmax state
-    __shared__ __attribute__((aligned(16))) bf16_t kv_lds[2 * KG * KT * KS_STRIDE];
+    __shared__ __attribute__((aligned(16))) bf16_t kv_lds[KG * KT * (KS_STRIDE + VS_STRIDE)];
     bf16_t *Ks = kv_lds, *Vs = kv_lds + KG * KT * KS_STRIDE;
 
     const AttnItem it = items[blockIdx.x];
@@ -158,9 +161,9 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         for (int q = 0; q < KG; ++q) {
 #pragma clang loop unroll(full)
             for (int i = 0; i < NLD; ++i) {
-                const int row = (q * KT + ((tid + 64 * WAVES * i) >> 4)) * KS_STRIDE + (tid & 15) * 8;
-                *reinterpret_cast<u32x4 *>(&Ks[row]) = kreg[q][i];
-                *reinterpret_cast<u32x4 *>(&Vs[row]) = vreg[q][i];
+                const int key = q * KT + ((tid + 64 * WAVES * i) >> 4);
+                *reinterpret_cast<u32x4 *>(&Ks[key * KS_STRIDE + (tid & 15) * 8]) = kreg[q][i];
+                *reinterpret_cast<u32x4 *>(&Vs[key * VS_STRIDE + (tid & 15) * 8]) = vreg[q][i];
             }
         }
         __syncthreads();
@@ -169,7 +172,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         }
         const int kt = kb0 + kg * KT;  // this key group's tile
         if (kt >= it.k1) continue;
-        const bf16_t *Kt = Ks + kg * KT * KS_STRIDE, *Vt = Vs + kg * KT * KS_STRIDE;
+        const bf16_t *Kt = Ks + kg * KT * KS_STRIDE, *Vt = Vs + kg * KT * VS_STRIDE;
         const bool full = kt + KT <= it.k1 && kt + KT - 1 <= minpos;  // no key of the tile is masked
 
         // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the tile
@@ -256,9 +259,9 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 // this lane addresses key ks*32 + 4g + m (then + 16), dims
                 // 16 nt + 4q .. +3, for m = (lane%16)/4, q = lane%4; it receives
                 // dim 16 nt + lane%16 of keys ks*32 + 4g + 0..3 and + 16 + 0..3
-                const bf16_t *vr = &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * KS_STRIDE + nt * 16 + 4 * (lane & 3)];
+                const bf16_t *vr = &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * VS_STRIDE + nt * 16 + 4 * (lane & 3)];
                 const i16x4 lo = lds_read_tr16(vr);
-                const i16x4 hi = lds_read_tr16(vr + 16 * KS_STRIDE);
+                const i16x4 hi = lds_read_tr16(vr + 16 * VS_STRIDE);
                 va[ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
 #pragma unroll
@@ -278,7 +281,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         // the second key group hands its state (per lane: O^T 32 values, m, l)
         // to the wavefront of the first group that holds the same pairs
         constexpr int ST = 34;
-        static_assert(WG * PPW * 64 * ST * 4 <= 2 * KG * KT * KS_STRIDE * 2, "merge area");
+        static_assert(WG * PPW * 64 * ST * 4 <= KG * KT * (KS_STRIDE + VS_STRIDE) * 2, "merge area");
         float *mg = reinterpret_cast<float *>(kv_lds);
         __syncthreads();  // every wavefront is done with the K/V tiles
         if (kg == 1) {
