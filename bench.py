@@ -34,7 +34,9 @@ WORKLOADS = {
     "qwen7b-k32": dict(shape="qwen2.5-7b", n=5000, span=16, K=32, policy="edit_local", lo=1000, hi=4000),
     "qwen7b-k128": dict(shape="qwen2.5-7b", n=5000, span=16, K=128, policy="edit_local", lo=1000, hi=4000),
     "qwen7b-k512": dict(shape="qwen2.5-7b", n=5000, span=16, K=512, policy="edit_local", lo=1000, hi=4000),
+    "qwen7b-random-k8": dict(shape="qwen2.5-7b", n=5000, span=16, K=8, policy="random", lo=1000, hi=4000),
     "qwen7b-random-k32": dict(shape="qwen2.5-7b", n=5000, span=16, K=32, policy="random", lo=1000, hi=4000),
+    "qwen7b-random-k128": dict(shape="qwen2.5-7b", n=5000, span=16, K=128, policy="random", lo=1000, hi=4000),
     "qwen7b-random-k512": dict(shape="qwen2.5-7b", n=5000, span=16, K=512, policy="random", lo=1000, hi=4000),
     "mistral7b-end": dict(shape="mistral-7b", n=5000, span=16, K=32, policy="edit_local", lo=4900, hi=4900),
     "mistral7b-start": dict(shape="mistral-7b", n=5000, span=16, K=32, policy="edit_local", lo=200, hi=200),
@@ -105,6 +107,29 @@ def repair_flops(shape, plans, span):
         f += 2 * len(P) * shape.n_layers * mat
         f += shape.n_layers * 4 * shape.n_heads * shape.head_dim * sum(p + 1 for p in P)
     return f
+
+
+def prefill_flops(shape, plans):
+    """Algorithmic flops of the same engine's full prefill of every document:
+    2 per weight element per position, and per layer 4 * H_q * head_dim * (p + 1)
+    of causal attention for the position p."""
+    mat = shape.layer_params() - 2 * shape.d_model - (shape.q_dim + 2 * shape.kv_dim if shape.qkv_bias else 0)
+    f = 0
+    for n, _, _ in plans:
+        f += 2 * n * shape.n_layers * mat
+        f += shape.n_layers * 4 * shape.n_heads * shape.head_dim * n * (n + 1) // 2
+    return f
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
@@ -233,7 +258,9 @@ def main():
         pev[i + 1].record(stream)
     torch.cuda.synchronize()
     prefill_ms = statistics.median([pev[i].elapsed_time(pev[i + 1]) for i in range(psteps)])
-    log(f"prefill of every edited context: median {prefill_ms:.2f} ms")
+    pflops = prefill_flops(shape, plans)
+    prefill_tflops = pflops / (prefill_ms * 1e-3) / 1e12
+    log(f"prefill of every edited context: median {prefill_ms:.2f} ms, {prefill_tflops:.0f} TFLOP/s algorithmic")
     del pcache
 
     steps_ms = {k: round(v[0] / args.steps, 4) for k, v in prof.items() if v[1]}
@@ -319,6 +346,13 @@ def main():
         "token_layers_per_s": round(R * L / (ms * 1e-3), 1),
         "prefill_ms": round(prefill_ms, 3),
         "speedup_vs_prefill": round(prefill_ms / ms, 2),
+        # the prefill is MFMA-bound: its algorithmic rate against the bf16 peak,
+        # and the issued rate (every product of a compensated operand pair is
+        # two MFMAs, so issued = 2 x algorithmic)
+        "prefill_algorithmic_flops": pflops,
+        "prefill_tflops": round(prefill_tflops, 1),
+        "prefill_mfma_frac": round(prefill_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "prefill_issued_mfma_frac": round(2 * prefill_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "token_layer_proxy_speedup": round(sum(n for n, _, _ in plans) / R, 2),
         "kernel_ms_per_repair_by_step": steps_ms,
         "profiled_loop_ms": round(profiled_ms, 4),
@@ -478,18 +512,22 @@ def cpu_baseline(shape, w, n, e, span, A, layers, n_docs, torch):
 
     stale = synth.make_stale_cache(shape, n, device="cuda")[:layers].to(torch.float64).cpu().numpy()
     toks = synth.apply_edit(synth.make_tokens(n, shape.vocab), e, span, shape.vocab).numpy()
-    t0 = time.perf_counter()
-    od.repair(shape, HostWeights(), stale, toks, e, e + span, A, n_layers=layers)
-    dt = time.perf_counter() - t0
+    runs = []
+    for _ in range(3):
+        work = stale.copy()
+        t0 = time.perf_counter()
+        od.repair(shape, HostWeights(), work, toks, e, e + span, A, n_layers=layers)
+        runs.append(time.perf_counter() - t0)
+    dt = statistics.median(runs)
     per_repair_ms = dt * 1e3 * shape.n_layers / layers * n_docs
-    log(f"cpu baseline: {dt:.2f} s for {layers} layers -> {per_repair_ms:.0f} ms per repair")
+    log(f"cpu baseline: {[round(r, 2) for r in runs]} s for {layers} layers -> median {per_repair_ms:.0f} ms per repair")
     return {"value": round(per_repair_ms, 1), "unit": "ms/repair", "cores": threads, "kind": "oracle",
-            "host_cpus": os.cpu_count(),
+            "blas_threads": threads, "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
+            "runs_s": [round(r, 3) for r in runs],
             "sample": f"fp64 numpy oracle repair of layers 0-{layers - 1} of {shape.n_layers} ({span + len(A)} rows, "
-                      f"n={n}, bf16->fp64 weight upcast included), scaled x{shape.n_layers / layers * n_docs:g}"
-                      f"{' (layers x documents)' if n_docs > 1 else ''}; "
-                      f"{dt:.1f} s measured"}
-
+                      f"n={n}, bf16->fp64 weight upcast included), median of 3 runs, scaled "
+                      f"x{shape.n_layers / layers * n_docs:g}{' (layers x documents)' if n_docs > 1 else ''}; "
+                      f"median run {dt:.1f} s"}
 
 if __name__ == "__main__":
     main()

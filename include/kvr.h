@@ -154,10 +154,12 @@ typedef struct {
  * stale elsewhere.  Slots outside P are never written.  Upstream positions
  * (< edit_start) are accepted (the full-position endpoint, Eq. 1, needs
  * them); policies select only downstream positions (kvr_select).
- * Documents are independent; they are batched into one pass per layer.
+ * Documents are independent; they are batched into one pass per layer, so
+ * their caches must not overlap (the byte ranges [d_cache, d_cache +
+ * kvr_cache_bytes(n_cap)) of the documents with a non-empty P are disjoint).
  * A document with an empty span and no positions is a no-op.
  * Errors: KVR_E_ARG (NULL pointers, unsorted/duplicate positions, positions
- * inside the span), KVR_E_RANGE (span or position outside [0, n), n > n_cap,
+ * inside the span, overlapping caches), KVR_E_RANGE (span or position outside [0, n), n > n_cap,
  * n_cap > max_ctx, sum of |P| > max_rows). */
 kvr_status kvr_repair(kvr_ctx *ctx, const kvr_doc *docs, int32_t n_docs, void *stream);
 
@@ -204,6 +206,36 @@ kvr_status kvr_score(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, cons
  * KVR_E_RANGE unless 1 <= q, 1 <= max_new and n + q + max_new - 1 <= n_cap. */
 kvr_status kvr_generate(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap, int32_t *d_tokens, int32_t q,
                         int32_t max_new, void *stream);
+
+/* Repair metrics on the host (Section 3, "What counts as repaired"; no
+ * context, no device).  For a cache state x the margin m_x is the
+ * length-averaged teacher-forced log-probability of the post-edit answer
+ * minus that of the pre-edit answer.
+ *
+ * kvr_answer_logprob: the mean log-probability of the answer_len answer
+ * tokens of a block scored by kvr_score as query_len query tokens followed by
+ * the answer; h_logprob is kvr_score's d_logprob copied to the host
+ * (n_logprob entries; entry j predicts appended token j+1, so the answer is
+ * predicted by entries query_len-1 .. query_len+answer_len-2).
+ * Errors: KVR_E_ARG (NULL), KVR_E_RANGE (query_len < 1, answer_len < 1, or
+ * the answer not inside the block). */
+kvr_status kvr_answer_logprob(const float *h_logprob, int32_t n_logprob, int32_t query_len, int32_t answer_len,
+                              double *out);
+
+/* Eq. 2, margin recovery (unclipped): *out = (m_repaired - m_stale) /
+ * (m_oracle - m_stale) and *defined = 1, or *out = 0 and *defined = 0 when the
+ * stale-to-oracle gap is zero (such items are left out of the mean).
+ * Errors: KVR_E_ARG (NULL outputs). */
+kvr_status kvr_margin_recovery(double m_repaired, double m_stale, double m_oracle, double *out, int32_t *defined);
+
+/* Eq. 3 for one item: *out = 1 when the post-edit answer h_a_new occurs in the
+ * greedy continuation (from kvr_generate) as a contiguous token run and the
+ * pre-edit answer h_a_old does not, else 0; the flip rate is the mean over
+ * the retained items.  An empty answer occurs in every continuation.
+ * Errors: KVR_E_ARG (NULL array with a positive length, negative lengths,
+ * NULL out). */
+kvr_status kvr_flipped(const int32_t *h_continuation, int32_t n_continuation, const int32_t *h_a_new, int32_t n_new,
+                       const int32_t *h_a_old, int32_t n_old, int32_t *out);
 
 /* CacheBlend selector (Table 1: top-K by the key/value deviation of one early
  * layer; Section 3, "Cost accounting": about one prefill layer over the

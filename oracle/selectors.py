@@ -2,8 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY; float64; shares no code with the library.
 
-Attention (Table 1: "top-K by stale-cache attention from the query"; Section
-3, "Cost accounting": a stale-cache scoring pass).  Readings (the paper's
+Attention (Table 1: the K pool positions that the query attends to most over
+the stale cache; Section 3, "Cost accounting": it costs one scoring pass over
+the stale cache).  Readings (the paper's
 appendix with the aggregation rule is not available):
 * the query tokens are appended after the n stale positions and run through
   the decoder as in the scoring forward (they attend over the stale cache and
@@ -14,9 +15,10 @@ appendix with the aggregation rule is not available):
 * top-K over the pool D by decreasing score, ties to the lower position,
   ascending.
 
-CacheBlend (Table 1: "top-K by layer-2 key/value deviation"; Section 3, "Cost
-accounting": it adds roughly one prefill layer over the prefix).  Readings:
-* "layer 2" counts from one, i.e. layer index 1: its keys/values need the
+CacheBlend (Table 1: the K pool positions whose keys/values of the second
+layer moved most; Section 3, "Cost accounting": its extra cost is about one
+prefill layer).  Readings:
+* the second layer counts from one, i.e. layer index 1: its keys/values need the
   full first layer over the changed suffix plus one projection, which is the
   stated cost of about one prefill layer (index 2 would cost two);
 * the fresh keys/values of the positions from the edit start to the end are

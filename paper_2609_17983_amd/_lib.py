@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPO
 
 EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
             "kvr_select", "kvr_select_to_boundary", "kvr_transplant", "kvr_score", "kvr_generate", "kvr_select_cacheblend",
-            "kvr_select_attention",
+            "kvr_select_attention", "kvr_answer_logprob", "kvr_margin_recovery", "kvr_flipped",
             "kvr_profile_enable", "kvr_profile_read", "kvr_last_error")
 
 
@@ -102,6 +102,13 @@ def load() -> ctypes.CDLL:
     lib.kvr_select_attention.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_int32, c_int32, c_int32,
                                          c_int32, c_void_p, c_void_p, POINTER(c_int32), c_void_p]
     lib.kvr_select_attention.restype = c_int
+    lib.kvr_answer_logprob.argtypes = [POINTER(c_float), c_int32, c_int32, c_int32, POINTER(c_double)]
+    lib.kvr_answer_logprob.restype = c_int
+    lib.kvr_margin_recovery.argtypes = [c_double, c_double, c_double, POINTER(c_double), POINTER(c_int32)]
+    lib.kvr_margin_recovery.restype = c_int
+    lib.kvr_flipped.argtypes = [POINTER(c_int32), c_int32, POINTER(c_int32), c_int32, POINTER(c_int32), c_int32,
+                                POINTER(c_int32)]
+    lib.kvr_flipped.restype = c_int
     lib.kvr_profile_enable.argtypes = [c_void_p, c_int32]
     lib.kvr_profile_enable.restype = c_int
     lib.kvr_profile_read.argtypes = [c_void_p, c_int32, POINTER(c_char_p), POINTER(c_double), POINTER(c_int64),
@@ -225,3 +232,29 @@ def kvr_select_attention(ctx: int, d_cache: int, n: int, n_cap: int, d_tokens: i
     _check(load().kvr_select_attention(ctx, d_cache, n, n_cap, d_tokens, q, edit_start, edit_end, K, d_out,
                                        d_mass_out, ctypes.byref(cnt), stream), ctx)
     return cnt.value
+
+
+def kvr_answer_logprob(logprob: Sequence[float], query_len: int, answer_len: int) -> float:
+    """Mean log p of the answer tokens of a block scored as query + answer
+    (logprob: kvr_score's output copied to the host)."""
+    arr = (c_float * max(1, len(logprob)))(*logprob)
+    out = c_double(0.0)
+    _check(load().kvr_answer_logprob(arr, len(logprob), query_len, answer_len, ctypes.byref(out)))
+    return out.value
+
+
+def kvr_margin_recovery(m_repaired: float, m_stale: float, m_oracle: float) -> Optional[float]:
+    """Eq. 2 (unclipped); None when the stale-to-oracle gap is zero."""
+    out = c_double(0.0)
+    defined = c_int32(0)
+    _check(load().kvr_margin_recovery(m_repaired, m_stale, m_oracle, ctypes.byref(out), ctypes.byref(defined)))
+    return out.value if defined.value else None
+
+
+def kvr_flipped(continuation: Sequence[int], a_new: Sequence[int], a_old: Sequence[int]) -> bool:
+    """Eq. 3 for one item: a_new occurs in the greedy continuation and a_old does not."""
+    arrs = [(c_int32 * max(1, len(x)))(*x) for x in (continuation, a_new, a_old)]
+    out = c_int32(0)
+    _check(load().kvr_flipped(arrs[0], len(continuation), arrs[1], len(a_new), arrs[2], len(a_old),
+                              ctypes.byref(out)))
+    return bool(out.value)

@@ -15,7 +15,7 @@ BUILD = os.path.join(os.path.dirname(PKG), "_build")
 LIB = os.path.join(PKG, "libkvr.so")
 
 SOURCES = ["engine.hip", "kernels_basic.hip", "gemm_skinny.hip", "gemm_tiled.hip", "attention.hip", "pack.hip",
-           "scoring.hip", "select_gpu.hip", "select.cpp"]
+           "scoring.hip", "select_gpu.hip", "select.cpp", "metrics.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-mcode-object-version=5", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",

@@ -1088,6 +1088,23 @@ kvr_status kvr_repair(kvr_ctx *c, const kvr_doc *docs, int32_t n_docs, void *str
     }
     if (total > c->d.max_rows) return fail(c, KVR_E_RANGE, "kvr_repair: total |P| exceeds max_rows");
     if (total == 0) return KVR_OK;
+    // Documents of one call are repaired in one pass: every document's fresh
+    // rows of a layer are scattered before any row attends.  Two documents
+    // sharing cache memory would then read each other's fresh rows, which two
+    // separate repairs would not, so overlapping caches are rejected.
+    {
+        std::vector<std::pair<uintptr_t, uintptr_t>> spans;
+        for (int i = 0; i < n_docs; ++i) {
+            const kvr_doc &dc = docs[i];
+            if ((dc.edit_end - dc.edit_start) + dc.n_positions == 0) continue;
+            const uintptr_t b = (uintptr_t)dc.d_cache;
+            spans.push_back({b, b + kvr_cache_bytes(&c->d, dc.n_cap)});
+        }
+        std::sort(spans.begin(), spans.end());
+        for (size_t i = 1; i < spans.size(); ++i)
+            if (spans[i].first < spans[i - 1].second)
+                return fail(c, KVR_E_ARG, "kvr_repair: two documents share cache memory");
+    }
 
     Tables t;
     t.rows.reserve((size_t)total);

@@ -168,11 +168,35 @@ def test_select_to_boundary_errors():
 
 
 def test_metrics_closed_forms():
-    from paper_2609_17983_amd import metrics
-    assert metrics.answer_logprob([-9.0, -1.0, -2.0, -3.0, -7.0], 2, 3) == -2.0
-    assert metrics.margin(-1.0, -3.0) == 2.0
-    assert metrics.margin_recovery(3.0, 1.0, 5.0) == 0.5
-    assert metrics.margin_recovery(-1.0, 1.0, 5.0) == -0.5
-    assert metrics.margin_recovery(2.0, 1.0, 1.0) is None
-    assert metrics.flipped([5, 6, 7, 8], [6, 7], [9]) and not metrics.flipped([5, 6, 7, 8], [6, 7], [8])
-    assert metrics.flip_rate([([1, 2], [2], [3]), ([1, 2], [3], [1])]) == 0.5
+    """Eq. 2 / Eq. 3 helpers of the library: closed-form cases, then random
+    cases against the oracle's own formulas (oracle/scoring.py)."""
+    from oracle import scoring as osc
+    assert kvr.kvr_answer_logprob([-9.0, -1.0, -2.0, -3.0, -7.0], 2, 3) == -2.0
+    assert kvr.kvr_margin_recovery(3.0, 1.0, 5.0) == 0.5
+    assert kvr.kvr_margin_recovery(-1.0, 1.0, 5.0) == -0.5
+    assert kvr.kvr_margin_recovery(2.0, 1.0, 1.0) is None
+    assert kvr.kvr_flipped([5, 6, 7, 8], [6, 7], [9]) and not kvr.kvr_flipped([5, 6, 7, 8], [6, 7], [8])
+    assert kvr.kvr_flipped([1, 2], [], [3]) and not kvr.kvr_flipped([1, 2], [2], [])
+    with pytest.raises(kvr.KvrError) as e:
+        kvr.kvr_answer_logprob([-1.0, -2.0], 2, 2)  # the answer runs past the block
+    assert e.value.status == kvr.KVR_E_RANGE
+    lib = kvr.load()
+    assert lib.kvr_flipped(None, 3, None, 0, None, 0, None) == kvr.KVR_E_ARG
+    assert lib.kvr_margin_recovery(1.0, 0.0, 2.0, None, None) == kvr.KVR_E_ARG
+    rnd = random.Random(3)
+    for _ in range(200):
+        lp = [rnd.uniform(-12.0, 0.0) for _ in range(rnd.randint(2, 30))]
+        q = rnd.randint(1, len(lp))
+        k = rnd.randint(1, len(lp) - q + 1)
+        # the C side sums float32 inputs in double, in order
+        import numpy as np
+        lp32 = np.asarray(lp, dtype=np.float32).astype(np.float64)
+        assert abs(kvr.kvr_answer_logprob(lp, q, k) - osc.mean_answer_logprob(lp32, q, k)) < 1e-12
+        m = [rnd.choice([rnd.uniform(-5, 5), 1.0]) for _ in range(3)]
+        ref = osc.margin_recovery(*m)
+        got = kvr.kvr_margin_recovery(*m)
+        assert (got is None and ref is None) or abs(got - ref) < 1e-12
+        y = [rnd.randint(0, 5) for _ in range(rnd.randint(0, 16))]
+        a = [rnd.randint(0, 5) for _ in range(rnd.randint(0, 3))]
+        b = [rnd.randint(0, 5) for _ in range(rnd.randint(0, 3))]
+        assert kvr.kvr_flipped(y, a, b) == osc.flip(y, a, b)

@@ -7,7 +7,8 @@ benchmark times (one kvr_repair call over the whole position set).
   with the oracle.  Prefill at n=5000 is checked on its first 32 rows (which
   depend only on the first 32 tokens) and, at any size, by the endpoint
   property (repairing every position equals prefill).
-* Qwen2.5-7B shape (QKV bias, 28/4 heads): EditLocal K=32 and Random K=512.
+* Qwen2.5-7B shape (QKV bias, 28/4 heads): K in {8, 32, 128, 512} for both
+  EditLocal and Random (seed 0), and Random K=32 at seeds 1-4.
 * Mistral-7B shape: edit near the end (4900) and near the start (200).
 * Batched repair, Llama-3-8B shape: 64 documents of 2000-8000 tokens, each with
   its own 16-token edit and EditLocal K=32, in one call (3072 rows); two
@@ -224,12 +225,22 @@ def qwen():
     _release(eng)
 
 
-@pytest.mark.parametrize("policy,K", [("edit_local", 32), ("random", 512)])
-def test_qwen7b_repair(qwen, policy, K):
+# The Qwen2.5-7B sweep: K in {8, 32, 128, 512} for the EditLocal window and
+# for the Random policy (seed 0), and the Random policy's other four seeds at
+# K = 32 (Table 1 runs it over five seeds).  Random sets scatter 8-512 rows
+# over [edit_end, n - 1): attention row blocks then span thousands of
+# positions and most key tiles take the masked path.
+QWEN_SWEEP = ([(p, K, 0) for p in ("edit_local", "random") for K in (8, 32, 128, 512)] +
+              [("random", 32, seed) for seed in (1, 2, 3, 4)])
+
+
+@pytest.mark.parametrize("policy,K,seed", QWEN_SWEEP, ids=[f"{p}-K{K}-seed{s}" for p, K, s in QWEN_SWEEP])
+def test_qwen7b_repair(qwen, policy, K, seed):
     e = synth.edit_position(1000, 4000)
     A = (osel.select_edit_local(N, e, e + SPAN, K) if policy == "edit_local"
-         else osel.select_random(N, e, e + SPAN, K, 0))
-    _full_repair(qwen, N, e, e + SPAN, A, tag=f"qwen7b edit@{e} {policy} K={K}")
+         else osel.select_random(N, e, e + SPAN, K, seed))
+    assert len(A) == K
+    _full_repair(qwen, N, e, e + SPAN, A, tag=f"qwen7b edit@{e} {policy} K={K} seed={seed}")
 
 
 @pytest.fixture(scope="module")

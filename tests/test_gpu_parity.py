@@ -224,8 +224,23 @@ def test_tiny_errors_leave_cache_untouched(tiny):
     assert e.value.status == kvr.KVR_E_RANGE
     with pytest.raises(kvr.KvrError):
         kvr.kvr_prefill(eng.ctx, t.data_ptr(), 0, 512, cache.data_ptr(), None, None)
+    # two documents over one cache (or overlapping parts of one allocation):
+    # one pass would let each read the other's fresh rows, so it is refused
+    flat = torch.zeros(2 * cache.numel(), dtype=cache.dtype, device="cuda")
+    inner = flat[1024:1024 + cache.numel()].view(cache.shape)
+    for pair in ((cache, cache), (flat[:cache.numel()].view(cache.shape), inner)):
+        with pytest.raises(kvr.KvrError) as e:
+            eng.repair([dict(cache=pair[0], tokens=t, edit_start=128, edit_end=136, positions=[]),
+                        dict(cache=pair[1], tokens=t, edit_start=200, edit_end=201, positions=[])])
+        assert e.value.status == kvr.KVR_E_ARG
+        assert "share cache memory" in kvr.kvr_last_error(eng.ctx)
+    # a document with nothing to repair may name any cache
+    eng.repair([dict(cache=flat[:cache.numel()].view(cache.shape), tokens=t, edit_start=128, edit_end=128,
+                     positions=[]),
+                dict(cache=inner, tokens=t, edit_start=128, edit_end=128, positions=[])])
     torch.cuda.synchronize()
     assert torch.equal(cache, before)
+    assert not flat.any()
 
 
 # ------------------------------------------------------------------------- mid bf16

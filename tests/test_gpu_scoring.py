@@ -16,7 +16,6 @@ import paper_2609_17983_amd as kvr
 import synth
 from oracle import decoder as od
 from oracle import scoring as osc
-from paper_2609_17983_amd import metrics
 from tests.gpu_util import TOL, Engine, OracleWeights, relmax, say, to_device_weights
 
 pytestmark = pytest.mark.gpu
@@ -115,8 +114,8 @@ def test_generate_matches_oracle():
         say(f"generate: {got} vs oracle {ref}")
         assert len(ref) >= 4 and got[:len(ref)] == ref
         # the metrics of Eq. 3 on these continuations
-        assert metrics.flipped(got, got[1:3], [shape.vocab + 1])
-        assert not metrics.flipped(got, got[1:3], got[2:4])
+        assert kvr.kvr_flipped(got, got[1:3], [shape.vocab + 1])
+        assert not kvr.kvr_flipped(got, got[1:3], got[2:4])
     finally:
         eng.close()
 

@@ -1,6 +1,7 @@
 """Pins for the oracle's CacheBlend selector (no GPU).
 
-Table 1 ("top-K by layer-2 key/value deviation") and Section 3: the fresh
+Table 1 (the K pool positions whose second-layer keys/values moved most) and
+Section 3: the fresh
 keys/values of one early layer are compared with the stale cache's.  Pinned
 by: the fresh states equal the full prefill of C' at that layer (the edit
 cannot change earlier positions), the deviation equals its definition taken
