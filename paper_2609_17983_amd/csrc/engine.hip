@@ -31,6 +31,22 @@ LaunchTimer &launch_timer() {
     return t;
 }
 
+// The host tables of one pass.  A context keeps one set, reserved to its
+// capacities when it is created, so that planning a pass allocates nothing.
+struct Tables {
+    struct Block { int doc, row0, nrows, kmax; };  // attention row block (planner)
+    std::vector<RowInfo> rows;
+    std::vector<DocInfo> docs;
+    std::vector<AttnItem> items;
+    std::vector<CombineItem> comb;
+    std::vector<Block> blocks;
+    int att_mt = 1;  // 16-row tiles per attention item (rows of a row block / 16)
+    void clear() {
+        rows.clear(); docs.clear(); items.clear(); comb.clear(); blocks.clear();
+        att_mt = 1;
+    }
+};
+
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -78,6 +94,7 @@ struct kvr_ctx {
     size_t attn_part_floats = 0;
     char *d_tables = nullptr;
     size_t tables_bytes = 0;
+    Tables tab;  // host tables of the pass being planned (capacity reserved at create)
 
     char *h_stage = nullptr;
     hipEvent_t stage_ev = nullptr;
@@ -142,14 +159,6 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 size_t elem_size(const kvr_dims &d) { return d.dtype == KVR_BF16 ? 2 : 4; }
 
-struct Tables {
-    std::vector<RowInfo> rows;
-    std::vector<DocInfo> docs;
-    std::vector<AttnItem> items;
-    std::vector<CombineItem> comb;
-    int att_mt = 1;  // 16-row tiles per attention item (rows of a row block / 16)
-};
-
 // Split the key ranges of the row blocks over work items: without splitting
 // when there are enough items to fill the GPU, otherwise in chunks of KS keys
 // (a multiple of the 64-key tile, at least two tiles) so that about `target`
@@ -160,8 +169,8 @@ struct Tables {
 void plan_attention(const kvr_ctx *c, Tables &t) {
     const int Hkv = c->d.n_kv_heads;
     const int G = c->d.n_heads / Hkv;
-    struct Block { int doc, row0, nrows, kmax; };
-    std::vector<Block> blocks;
+    using Block = Tables::Block;
+    std::vector<Block> &blocks = t.blocks;
     auto make_blocks = [&](int rows_blk) {
         blocks.clear();
         for (int di = 0; di < (int)t.docs.size(); ++di) {
@@ -224,9 +233,15 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
             next_slot += ns;
         }
     }
-    // longest key ranges first, so that short items fill the tail
-    std::stable_sort(t.items.begin(), t.items.end(),
-                     [](const AttnItem &x, const AttnItem &y) { return (x.k1 - x.k0) > (y.k1 - y.k0); });
+    // longest key ranges first, so that short items fill the tail; equal
+    // lengths keep the order they were made in (document, rows, kv head, keys),
+    // which is a total order, so the in-place sort is deterministic
+    std::sort(t.items.begin(), t.items.end(), [](const AttnItem &x, const AttnItem &y) {
+        if (x.k1 - x.k0 != y.k1 - y.k0) return (x.k1 - x.k0) > (y.k1 - y.k0);
+        if (x.row0 != y.row0) return x.row0 < y.row0;
+        if (x.kvh != y.kvh) return x.kvh < y.kvh;
+        return x.k0 < y.k0;
+    });
 }
 
 // Weight tiles per block and split-K factor of a skinny projection.  The X
@@ -550,7 +565,8 @@ kvr_status score_block(kvr_ctx *c, void *cache, int n, int n_cap, const int32_t 
                        int32_t *argmax, int32_t *next, hipStream_t s) {
     const kvr_dims &d = c->d;
     const int D = d.d_model, V = d.vocab;
-    Tables t;
+    Tables &t = c->tab;
+    t.clear();
     t.docs.push_back(DocInfo{cache, tokens, c->score_y, n + m, n_cap, 0, m});
     t.rows.reserve(m);
     for (int j = 0; j < m; ++j) t.rows.push_back(RowInfo{n + j, 0, j, 0});
@@ -692,6 +708,11 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     const int blocks_cap = c->rows_cap / 16 + c->max_docs + 1;
     c->items_cap = blocks_cap * d.n_kv_heads + max_slots;
     c->comb_cap = blocks_cap * d.n_kv_heads;
+    c->tab.rows.reserve(c->rows_cap);
+    c->tab.docs.reserve(c->max_docs);
+    c->tab.items.reserve(c->items_cap);
+    c->tab.comb.reserve(c->comb_cap);
+    c->tab.blocks.reserve(blocks_cap);
     c->tables_bytes = align_up((size_t)c->rows_cap * sizeof(RowInfo), 256) +
                       align_up((size_t)c->max_docs * sizeof(DocInfo), 256) +
                       align_up((size_t)c->items_cap * sizeof(AttnItem), 256) + (size_t)c->comb_cap * sizeof(CombineItem);
@@ -844,7 +865,8 @@ kvr_status kvr_prefill(kvr_ctx *c, const int32_t *d_tokens, int32_t n, int32_t n
     const int chunk = c->rows_cap;
     for (int c0 = 0; c0 < n; c0 += chunk) {
         const int c1 = std::min(n, c0 + chunk);
-        Tables t;
+        Tables &t = c->tab;
+        t.clear();
         t.docs.push_back(DocInfo{d_cache, d_tokens, d_hidden_out, n, n_cap, 0, c1 - c0});
         t.rows.reserve(c1 - c0);
         for (int p = c0; p < c1; ++p) t.rows.push_back(RowInfo{p, 0, p, 0});
@@ -958,70 +980,91 @@ kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int
     const size_t cache_bytes = align_up((size_t)(layer + 1) * 2 * d.n_kv_heads * n_cap * row, 256);
     kvr_status st0 = sel_reserve(c, cache_bytes + (size_t)n_cap * 4, s, "kvr_select_cacheblend");
     if (st0 != KVR_OK) return st0;
-    char *scratch = c->sel_scratch;
-    float *dev = d_dev_out ? d_dev_out : (float *)(scratch + cache_bytes);
+    char *work = c->sel_scratch;  // scratch cache copy, then the deviations
+    float *dev = d_dev_out ? d_dev_out : (float *)(work + cache_bytes);
     // layers below `layer`, positions before the edit: the stale states (the
     // edit does not reach them) for the suffix forward to attend over
     if (layer > 0 && edit_start > 0) {
-        hipError_t e = hipMemcpy2DAsync(scratch, (size_t)n_cap * row, d_cache, (size_t)n_cap * row,
+        hipError_t e = hipMemcpy2DAsync(work, (size_t)n_cap * row, d_cache, (size_t)n_cap * row,
                                         (size_t)edit_start * row, (size_t)layer * 2 * d.n_kv_heads,
                                         hipMemcpyDeviceToDevice, s);
         if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: hipMemcpy2DAsync");
     }
     // the suffix [edit_start, n) of C' through layers 0..layer-1 and the
-    // key/value projection of `layer`, into the scratch cache
+    // key/value projection of `layer`, into the work cache
     for (int c0 = edit_start; c0 < n; c0 += c->rows_cap) {
         const int c1 = std::min(n, c0 + c->rows_cap);
-        Tables t;
-        t.docs.push_back(DocInfo{scratch, d_tokens_new, nullptr, n, n_cap, 0, c1 - c0});
+        Tables &t = c->tab;
+        t.clear();
+        t.docs.push_back(DocInfo{work, d_tokens_new, nullptr, n, n_cap, 0, c1 - c0});
         t.rows.reserve(c1 - c0);
         for (int p = c0; p < c1; ++p) t.rows.push_back(RowInfo{p, 0, p - c0, 0});
         kvr_status st = run_pass(c, t, s, layer);
         if (st != KVR_OK) return st;
     }
-    hipError_t e = launch_kv_deviation(c->bf16, scratch, n_cap, layer, d_cache, n_cap, layer, d.n_kv_heads,
+    hipError_t e = launch_kv_deviation(c->bf16, work, n_cap, layer, d_cache, n_cap, layer, d.n_kv_heads,
                                        d.head_dim, edit_end, n - 1, dev, s);
     if (e == hipSuccess) e = launch_topk(dev, m, *n_out, edit_end, d_out, s);
     if (e != hipSuccess) return hip_fail(c, e, "kvr_select_cacheblend: deviation / top-K");
     return KVR_OK;
 }
 
-kvr_status kvr_select_attention(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens,
-                                int32_t q, int32_t edit_start, int32_t edit_end, int32_t K, int32_t *d_out,
-                                float *d_mass_out, int32_t *n_out, void *stream) {
-    if (!c) return fail(nullptr, KVR_E_ARG, "kvr_select_attention: NULL context");
+// Body of the Attention-selector entry point.  `buf` null: the scratch comes
+// from the context (grown on demand); otherwise `buf` holds `cap` bytes of
+// device scratch and nothing is allocated.
+static kvr_status select_attention(kvr_ctx *c, const char *who, void *d_cache, int32_t n, int32_t n_cap,
+                                   const int32_t *d_tokens, int32_t q, int32_t edit_start, int32_t edit_end,
+                                   int32_t K, int32_t *d_out, float *d_mass_out, int32_t *n_out, void *stream,
+                                   char *buf, size_t cap) {
+    if (!c) return fail(nullptr, KVR_E_ARG, std::string(who) + ": NULL context");
     if (!d_cache || !d_tokens || !n_out || K < 0 || (K > 0 && !d_out))
-        return fail(c, KVR_E_ARG, "kvr_select_attention: NULL argument or negative K");
-    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, "kvr_select_attention: cache must be 16-byte aligned");
+        return fail(c, KVR_E_ARG, std::string(who) + ": NULL argument or negative K");
+    if (!aligned16(d_cache)) return fail(c, KVR_E_ARG, std::string(who) + ": cache must be 16-byte aligned");
     if (n < 1 || q < 1 || (long long)n + q > n_cap || n_cap > c->d.max_ctx || edit_start < 0 ||
         edit_start > edit_end || edit_end > n)
-        return fail(c, KVR_E_RANGE, "kvr_select_attention: need 1 <= n, 1 <= q, n + q <= n_cap <= max_ctx and "
-                                    "0 <= edit_start <= edit_end <= n");
-    if (q > c->rows_cap) return fail(c, KVR_E_RANGE, "kvr_select_attention: query longer than one pass holds");
+        return fail(c, KVR_E_RANGE, std::string(who) + ": need 1 <= n, 1 <= q, n + q <= n_cap <= max_ctx and "
+                                                       "0 <= edit_start <= edit_end <= n");
+    if (q > c->rows_cap) return fail(c, KVR_E_RANGE, std::string(who) + ": query longer than one pass holds");
+    const kvr_dims &d = c->d;
+    const size_t part_bytes = align_up((size_t)d.n_kv_heads * n * 4, 256);
+    const size_t lse_bytes = align_up((size_t)q * d.n_heads * 4, 256);
+    const size_t need = part_bytes + lse_bytes + (d_mass_out ? 0 : (size_t)n * 4);
+    if (buf && need > cap)
+        return fail(c, KVR_E_RANGE, std::string(who) + ": needs " + std::to_string(need) +
+                                        " bytes of scratch, more than the fixed " + std::to_string(cap));
     const int m = std::max(0, n - 1 - edit_end);  // pool D = [edit_end, n - 1)
     *n_out = std::min(K, m);
     if (m == 0 && !d_mass_out) return KVR_OK;
     DeviceGuard g(c->device);
     hipStream_t s = (hipStream_t)stream;
-    const kvr_dims &d = c->d;
-    const size_t part_bytes = align_up((size_t)d.n_kv_heads * n * 4, 256);
-    const size_t lse_bytes = align_up((size_t)q * d.n_heads * 4, 256);
-    kvr_status st = sel_reserve(c, part_bytes + lse_bytes + (size_t)n * 4, s, "kvr_select_attention");
-    if (st != KVR_OK) return st;
-    MassHook mh{d_cache, n_cap, n, (float *)(c->sel_scratch + part_bytes), (float *)c->sel_scratch};
-    float *mass = d_mass_out ? d_mass_out : (float *)(c->sel_scratch + part_bytes + lse_bytes);
+    if (!buf) {
+        kvr_status st = sel_reserve(c, need, s, who);
+        if (st != KVR_OK) return st;
+        buf = c->sel_scratch;
+    }
+    // part [Hkv][n] is written (not accumulated) at layer 0 and lse at every
+    // layer before it is read, so the scratch needs no clearing
+    MassHook mh{d_cache, n_cap, n, (float *)(buf + part_bytes), (float *)buf};
+    float *mass = d_mass_out ? d_mass_out : (float *)(buf + part_bytes + lse_bytes);
     // the query rows at positions [n, n + q) over the stale cache (their own
     // keys/values land in slots [n, n + q))
-    Tables t;
+    Tables &t = c->tab;
+    t.clear();
     t.docs.push_back(DocInfo{d_cache, d_tokens, nullptr, n + q, n_cap, 0, q});
-    t.rows.reserve(q);
     for (int j = 0; j < q; ++j) t.rows.push_back(RowInfo{n + j, 0, j, 0});
-    st = run_pass(c, t, s, -1, &mh);
+    kvr_status st = run_pass(c, t, s, -1, &mh);
     if (st != KVR_OK) return st;
     hipError_t e = launch_mass_reduce(mh.part, d.n_kv_heads, n, mass, s);
     if (e == hipSuccess && m > 0) e = launch_topk(mass + edit_end, m, *n_out, edit_end, d_out, s);
-    if (e != hipSuccess) return hip_fail(c, e, "kvr_select_attention: reduce / top-K");
+    if (e != hipSuccess) return hip_fail(c, e, (std::string(who) + ": reduce / top-K").c_str());
     return KVR_OK;
+}
+
+kvr_status kvr_select_attention(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap, const int32_t *d_tokens,
+                                int32_t q, int32_t edit_start, int32_t edit_end, int32_t K, int32_t *d_out,
+                                float *d_mass_out, int32_t *n_out, void *stream) {
+    return select_attention(c, "kvr_select_attention", d_cache, n, n_cap, d_tokens, q, edit_start, edit_end, K,
+                            d_out, d_mass_out, n_out, stream, nullptr, 0);
 }
 
 kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {
@@ -1106,7 +1149,8 @@ kvr_status kvr_repair(kvr_ctx *c, const kvr_doc *docs, int32_t n_docs, void *str
                 return fail(c, KVR_E_ARG, "kvr_repair: two documents share cache memory");
     }
 
-    Tables t;
+    Tables &t = c->tab;
+    t.clear();
     t.rows.reserve((size_t)total);
     for (int i = 0; i < n_docs; ++i) {
         const kvr_doc &dc = docs[i];
