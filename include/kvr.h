@@ -280,6 +280,26 @@ kvr_status kvr_select_attention(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t 
                                 int32_t q, int32_t edit_start, int32_t edit_end, int32_t K, int32_t *d_out,
                                 float *d_mass_out, int32_t *n_out, void *stream);
 
+/* kvr_select_attention for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, semantics and errors as kvr_select_attention,
+ * with the selector's scratch (the per-kv-head mass [n_kv_heads][n], the
+ * query rows' log-sum-exp [q][n_heads] and, when d_mass_out is NULL, the mass
+ * [n]; each part rounded up to 256 bytes) in a fixed device array of
+ * 4 MiB (4194304 bytes) that the library holds on each device it runs on
+ * until the process ends, instead of a context buffer grown on first use.
+ * Nothing is allocated on the device or the host heap (with the step
+ * profiler off; kvr_create allocated the context beforehand).  Every call on
+ * one device shares that array: calls that overlap in time on one device
+ * (two streams, two contexts, two threads) race and give undefined results;
+ * calls ordered on one stream are independent (nothing in the array needs to
+ * start at zero).  Additional errors: KVR_E_RANGE when the scratch above
+ * exceeds 4 MiB (about n_kv_heads * n <= 1,000,000 with d_mass_out given);
+ * KVR_E_HIP if the array's device address could not be obtained. */
+kvr_status kvr_select_attention_noalloc(kvr_ctx *ctx, void *d_cache, int32_t n, int32_t n_cap,
+                                        const int32_t *d_tokens, int32_t q, int32_t edit_start, int32_t edit_end,
+                                        int32_t K, int32_t *d_out, float *d_mass_out, int32_t *n_out, void *stream);
+
 /* EditLocal@boundary (Section 5.2, "How Far the Window Should Extend"): the
  * structural variant that recomputes from the end of the edit to the next
  * document boundary, with no selector forward.  Returns the positions

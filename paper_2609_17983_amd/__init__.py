@@ -7,7 +7,7 @@ from ._lib import (KVR_BF16, KVR_E_ARG, KVR_E_HIP, KVR_E_NOMEM, KVR_E_RANGE, KVR
                    KVR_F32, KVR_OK, KVR_RANDOM, EXPORTED, LIB_PATH, KvrError, kvr_cache_bytes, kvr_create, kvr_destroy,
                    kvr_dims, kvr_doc, kvr_last_error, kvr_layer_weights, kvr_prefill, kvr_profile_enable,
                    kvr_profile_read, kvr_repair, kvr_select, kvr_select_to_boundary, kvr_transplant,
-                   kvr_score, kvr_generate, kvr_select_cacheblend, kvr_select_attention,
+                   kvr_score, kvr_generate, kvr_select_cacheblend, kvr_select_attention, kvr_select_attention_noalloc,
                    kvr_answer_logprob, kvr_margin_recovery, kvr_flipped,
                    kvr_weights, kvr_workspace_bytes, load, make_doc)
 from .marshal import dims_for, weights_struct
@@ -17,6 +17,7 @@ __all__ = [
     "KVR_F32", "KVR_OK", "KVR_RANDOM", "EXPORTED", "LIB_PATH", "KvrError", "kvr_cache_bytes", "kvr_create",
     "kvr_destroy", "kvr_dims", "kvr_doc", "kvr_last_error", "kvr_layer_weights", "kvr_prefill",
     "kvr_profile_enable", "kvr_profile_read", "kvr_repair", "kvr_select", "kvr_select_to_boundary",
-    "kvr_transplant", "kvr_score", "kvr_generate", "kvr_select_cacheblend", "kvr_select_attention", "kvr_answer_logprob",
+    "kvr_transplant", "kvr_score", "kvr_generate", "kvr_select_cacheblend", "kvr_select_attention", "kvr_select_attention_noalloc",
+    "kvr_answer_logprob",
     "kvr_margin_recovery", "kvr_flipped", "kvr_weights", "kvr_workspace_bytes", "load", "make_doc", "dims_for", "weights_struct",
 ]

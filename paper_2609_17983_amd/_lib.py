@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "KVR_OK", 1: "KVR_E_ARG", 2: "KVR_E_RANGE", 3: "KVR_E_UNSUPPO
 
 EXPORTED = ("kvr_create", "kvr_destroy", "kvr_cache_bytes", "kvr_workspace_bytes", "kvr_prefill", "kvr_repair",
             "kvr_select", "kvr_select_to_boundary", "kvr_transplant", "kvr_score", "kvr_generate", "kvr_select_cacheblend",
-            "kvr_select_attention", "kvr_answer_logprob", "kvr_margin_recovery", "kvr_flipped",
+            "kvr_select_attention", "kvr_select_attention_noalloc", "kvr_answer_logprob", "kvr_margin_recovery", "kvr_flipped",
             "kvr_profile_enable", "kvr_profile_read", "kvr_last_error")
 
 
@@ -102,6 +102,8 @@ def load() -> ctypes.CDLL:
     lib.kvr_select_attention.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_int32, c_int32, c_int32,
                                          c_int32, c_void_p, c_void_p, POINTER(c_int32), c_void_p]
     lib.kvr_select_attention.restype = c_int
+    lib.kvr_select_attention_noalloc.argtypes = lib.kvr_select_attention.argtypes
+    lib.kvr_select_attention_noalloc.restype = c_int
     lib.kvr_answer_logprob.argtypes = [POINTER(c_float), c_int32, c_int32, c_int32, POINTER(c_double)]
     lib.kvr_answer_logprob.restype = c_int
     lib.kvr_margin_recovery.argtypes = [c_double, c_double, c_double, POINTER(c_double), POINTER(c_int32)]
@@ -231,6 +233,17 @@ def kvr_select_attention(ctx: int, d_cache: int, n: int, n_cap: int, d_tokens: i
     cnt = c_int32(0)
     _check(load().kvr_select_attention(ctx, d_cache, n, n_cap, d_tokens, q, edit_start, edit_end, K, d_out,
                                        d_mass_out, ctypes.byref(cnt), stream), ctx)
+    return cnt.value
+
+
+def kvr_select_attention_noalloc(ctx: int, d_cache: int, n: int, n_cap: int, d_tokens: int, q: int,
+                                 edit_start: int, edit_end: int, K: int, d_out: Optional[int],
+                                 d_mass_out: Optional[int] = None, stream: Optional[int] = None) -> int:
+    """kvr_select_attention with its scratch in the library's fixed device array
+    (allocates nothing); returns the number of positions written to d_out."""
+    cnt = c_int32(0)
+    _check(load().kvr_select_attention_noalloc(ctx, d_cache, n, n_cap, d_tokens, q, edit_start, edit_end, K, d_out,
+                                               d_mass_out, ctypes.byref(cnt), stream), ctx)
     return cnt.value
 
 

@@ -13,6 +13,8 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -48,6 +50,15 @@ struct Tables {
 };
 
 }  // namespace kvr
+
+// Device scratch of kvr_select_attention_noalloc, a fixed file-scope array:
+// each device the library runs on holds one copy until the process ends, and
+// every call on that device shares it.  In host code `scratch` names a
+// host-side stand-in, not the device copy: its device address comes from
+// hipGetSymbolAddress, looked up once per device (scratch_address) and kept
+// in each context; only that address is passed to kernels.
+static constexpr size_t NOALLOC_SCRATCH_BYTES = 4u << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
 
 struct kvr_ctx {
     kvr_dims d{};
@@ -95,6 +106,8 @@ struct kvr_ctx {
     char *d_tables = nullptr;
     size_t tables_bytes = 0;
     Tables tab;  // host tables of the pass being planned (capacity reserved at create)
+    void *scratch_ptr = nullptr;        // this device's copy of `scratch` (kvr_select_attention_noalloc)
+    hipError_t scratch_err = hipSuccess;
 
     char *h_stage = nullptr;
     hipEvent_t stage_ev = nullptr;
@@ -142,6 +155,22 @@ kvr_status fail(kvr_ctx *c, kvr_status st, const std::string &msg) {
 
 kvr_status hip_fail(kvr_ctx *c, hipError_t e, const char *what) {
     return fail(c, KVR_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (hipGetSymbolAddress with that device current) and kept.
+hipError_t scratch_address(int device, void **out) {
+    static std::mutex mu;
+    static std::map<int, std::pair<void *, hipError_t>> table;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = table.find(device);
+    if (it == table.end()) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        it = table.emplace(device, std::make_pair(e == hipSuccess ? ptr : nullptr, e)).first;
+    }
+    *out = it->second.first;
+    return it->second.second;
 }
 
 struct DeviceGuard {
@@ -695,6 +724,9 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     c->lm_head = wts->lm_head ? wts->lm_head : wts->embed;
     hipError_t e = hipGetDevice(&c->device);
     if (e != hipSuccess) { delete c; return hip_fail(nullptr, e, "hipGetDevice"); }
+    // the no-allocation selector's scratch on this (current) device; a failed
+    // lookup only disables that entry point
+    c->scratch_err = scratch_address(c->device, &c->scratch_ptr);
 
     const int D = d.d_model, F = d.d_ffn, hd = d.head_dim;
     const int qd = d.n_heads * hd, kd = d.n_kv_heads * hd;
@@ -1009,9 +1041,9 @@ kvr_status kvr_select_cacheblend(kvr_ctx *c, const void *d_cache, int32_t n, int
     return KVR_OK;
 }
 
-// Body of the Attention-selector entry point.  `buf` null: the scratch comes
-// from the context (grown on demand); otherwise `buf` holds `cap` bytes of
-// device scratch and nothing is allocated.
+// Shared body of the two Attention-selector entry points.  `buf` null: the
+// scratch comes from the context (grown on demand); otherwise `buf` holds
+// `cap` bytes of device scratch and nothing is allocated.
 static kvr_status select_attention(kvr_ctx *c, const char *who, void *d_cache, int32_t n, int32_t n_cap,
                                    const int32_t *d_tokens, int32_t q, int32_t edit_start, int32_t edit_end,
                                    int32_t K, int32_t *d_out, float *d_mass_out, int32_t *n_out, void *stream,
@@ -1065,6 +1097,17 @@ kvr_status kvr_select_attention(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_
                                 float *d_mass_out, int32_t *n_out, void *stream) {
     return select_attention(c, "kvr_select_attention", d_cache, n, n_cap, d_tokens, q, edit_start, edit_end, K,
                             d_out, d_mass_out, n_out, stream, nullptr, 0);
+}
+
+kvr_status kvr_select_attention_noalloc(kvr_ctx *c, void *d_cache, int32_t n, int32_t n_cap,
+                                        const int32_t *d_tokens, int32_t q, int32_t edit_start, int32_t edit_end,
+                                        int32_t K, int32_t *d_out, float *d_mass_out, int32_t *n_out, void *stream) {
+    if (c && !c->scratch_ptr)
+        return fail(c, KVR_E_HIP, std::string("kvr_select_attention_noalloc: the device scratch has no address (") +
+                                      hipGetErrorString(c->scratch_err) + ")");
+    return select_attention(c, "kvr_select_attention_noalloc", d_cache, n, n_cap, d_tokens, q, edit_start, edit_end,
+                            K, d_out, d_mass_out, n_out, stream, (char *)(c ? c->scratch_ptr : nullptr),
+                            NOALLOC_SCRATCH_BYTES);
 }
 
 kvr_status kvr_profile_enable(kvr_ctx *c, int32_t enable) {
