@@ -133,6 +133,7 @@ struct LinearArgs {
     int32_t ldo;
     int32_t split;        // tiled STORE only: K cut into `split` slices, partial
                           // tiles out[s][R][ldo] summed by the consumer (<= 1: none)
+    int32_t group_all;    // tiled: at most this many row blocks form one group of the tile order (set by the launcher)
 };
 
 // Skinny (R <= 64) linear layer: X in operand order, W packed in operand order

@@ -30,11 +30,13 @@
 //
 // Tile order.  Workgroups are handed to the eight XCDs in turn (workgroup b to
 // XCD b % 8), and each XCD has its own L2.  The output tiles are therefore
-// numbered in groups of four row blocks (within a group: column block outer,
-// row block inner), the numbering is cut into eight contiguous ranges, and
-// XCD x runs range x in order: the blocks an XCD runs together cover about
-// four row blocks by eight column blocks, whose activation and weight slabs
-// its L2 shares.
+// numbered in groups of row blocks (within a group: column block outer, row
+// block inner), the numbering is cut into eight contiguous ranges, and XCD x
+// runs range x in order, so the blocks that read one weight slab run at the
+// same time on one XCD and share its L2.  Up to GROUP_ALL row blocks form one
+// group (a repair of a few hundred rows: every weight slab is fetched from
+// HBM about once; with groups of four, 528 rows fetched 3.6 times the
+// gate/up weights); more (prefill, batches) are grouped by four.
 #include <stdlib.h>
 
 #include <algorithm>
@@ -48,7 +50,8 @@ namespace {
 constexpr int WT = 16;          // 16-row weight tiles per block (256 output columns)
 constexpr int FRAG = 512;       // bf16 elements of one 16 x 32 operand fragment
 constexpr int XCDS = 8;         // L2 domains the workgroups are dealt to in turn
-constexpr int GROUP_M = 4;      // row blocks per group of the tile order
+constexpr int GROUP_M = 4;      // row blocks per group of the tile order (many row blocks)
+constexpr int GROUP_ALL = 12;   // up to this many row blocks, one group holds them all
 
 // Block shape for RT 16-row activation tiles: wavefronts in WM rows x WN
 // columns, each owning 4 row tiles x JT weight tiles (64 x 128 or 64 x 64).
@@ -114,10 +117,11 @@ __global__ __launch_bounds__(64 * TileShape<RT>::NW, TileShape<RT>::BLOCKS_PER_C
     const int T = MB * NB, per = (T + XCDS - 1) / XCDS;
     const int tile = (blockIdx.x % XCDS) * per + blockIdx.x / XCDS;
     if (tile >= T) return;
-    const int grp = tile / (GROUP_M * NB);
-    const int gm = min(GROUP_M, MB - grp * GROUP_M);
-    const int ti = tile - grp * GROUP_M * NB;
-    const int bn = ti / gm, bm = grp * GROUP_M + ti % gm;
+    const int GM = MB <= a.group_all ? MB : GROUP_M;
+    const int grp = tile / (GM * NB);
+    const int gm = min(GM, MB - grp * GM);
+    const int ti = tile - grp * GM * NB;
+    const int bn = ti / gm, bm = grp * GM + ti % gm;
 
     // this wavefront's fragments of every k-step: f = FPW w + i (X hi row
     // tiles, X lo row tiles, then weight tiles).  The array has a fixed size:
@@ -279,9 +283,12 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s) {
     if (a.split > 1 && (epi != EPI_STORE || a.split > a.K / 32)) return hipErrorInvalidValue;
     const int rt = tiled_rt(a.R, vrows);
     const int blocks = tiled_blocks(a.R, vrows, nullptr);
-    if (rt == 16) launch_rt<16>(epi, a, blocks, s);
-    else if (rt == 8) launch_rt<8>(epi, a, blocks, s);
-    else launch_rt<4>(epi, a, blocks, s);
+    LinearArgs b = a;
+    const char *ge = getenv("KVR_TILED_GROUP");  // tuning: row blocks that may form one group
+    b.group_all = ge && *ge ? atoi(ge) : GROUP_ALL;
+    if (rt == 16) launch_rt<16>(epi, b, blocks, s);
+    else if (rt == 8) launch_rt<8>(epi, b, blocks, s);
+    else launch_rt<4>(epi, b, blocks, s);
     return hipGetLastError();
 }
 
