@@ -175,24 +175,35 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         const bf16_t *Kt = Ks + kg * KT * KS_STRIDE, *Vt = Vs + kg * KT * VS_STRIDE;
         const bool full = kt + KT <= it.k1 && kt + KT - 1 <= minpos;  // no key of the tile is masked
 
-        // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the tile
+        // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the
+        // tile.  All sixteen key fragments are read from LDS first, then the
+        // MFMAs run k-step-major over the four accumulators, so that no MFMA
+        // waits for an LDS round trip or for the one before it in its chain
+        // (read, wait, two dependent MFMAs per fragment made the tile a chain of
+        // LDS latencies).  Each accumulator still sums hi, lo of k-step 0, then
+        // of k-step 1, ...
         f32x4 s[PPW][4];
+        bf16x8 kb[4][4];
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            bf16x8 kb[4];
+        for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kb[ks] = ld16(&Kt[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
+            for (int ks = 0; ks < 4; ++ks) kb[nt][ks] = ld16(&Kt[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
+#pragma unroll
+        for (int i = 0; i < PPW; ++i)
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
             for (int i = 0; i < PPW; ++i) {
-                s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
                 if (!pvalid[i]) continue;
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks], qv[i][ks], s[i][nt], 0, 0, 0);
-                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks], ql[i][ks], s[i][nt], 0, 0, 0);
-                }
+                for (int nt = 0; nt < 4; ++nt)
+                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], qv[i][ks], s[i][nt], 0, 0, 0);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], ql[i][ks], s[i][nt], 0, 0, 0);
             }
-        }
         // online softmax, one query row per lane column
         bf16x8 pb[PPW][2], pl[PPW][2];
 #pragma unroll
@@ -250,10 +261,12 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 pl[i][ks] = __builtin_bit_cast(bf16x8, v);
             }
         }
-        // O^T += V^T P^T: A operand = V^T rows (dims 16*nt + lane%16) over the same key slots
+        // O^T += V^T P^T: A operand = V^T rows (dims 16*nt + lane%16) over the
+        // same key slots; as above, every fragment is read first and the MFMAs
+        // of the eight accumulators then interleave (same per-accumulator order)
+        bf16x8 va[8][2];
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt) {
-            bf16x8 va[2];
+        for (int nt = 0; nt < 8; ++nt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 // this lane addresses key ks*32 + 4g + m (then + 16), dims
@@ -262,18 +275,20 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
                 const bf16_t *vr = &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * VS_STRIDE + nt * 16 + 4 * (lane & 3)];
                 const i16x4 lo = lds_read_tr16(vr);
                 const i16x4 hi = lds_read_tr16(vr + 16 * VS_STRIDE);
-                va[ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                va[nt][ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
             for (int i = 0; i < PPW; ++i) {
                 if (!pvalid[i]) continue;
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks], pb[i][ks], oacc[i][nt], 0, 0, 0);
-                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[ks], pl[i][ks], oacc[i][nt], 0, 0, 0);
-                }
+                for (int nt = 0; nt < 8; ++nt)
+                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pb[i][ks], oacc[i][nt], 0, 0, 0);
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt)
+                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pl[i][ks], oacc[i][nt], 0, 0, 0);
             }
-        }
     }
 #undef KVR_ATT_FETCH
 
