@@ -134,11 +134,17 @@ __global__ __launch_bounds__(256) void linear_skinny_kernel(SkinnyArgs a) {
 #pragma unroll
         for (int j = 0; j < D; ++j) load(j, phys(s0 + j));
         int s = s0;
+        // The scheduling barriers keep each slot's refill right behind its
+        // MFMAs: left free, the compiler sank every refill below the MFMAs of
+        // all slots and waited for nearly every load before issuing the next
+        // batch, so the ring drained once per pass through it.
         for (; s + D <= s1; s += D) {
 #pragma unroll
             for (int j = 0; j < D; ++j) {
                 mma(j);
+                __builtin_amdgcn_sched_barrier(0);
                 load(j, phys(s + j + D));
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         // fewer than D k-steps remain, already in the ring
