@@ -176,34 +176,41 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
         const bool full = kt + KT <= it.k1 && kt + KT - 1 <= minpos;  // no key of the tile is masked
 
         // S^T = K Q^T: lane holds query row lane%16, keys 16*nt + 4*g + e of the
-        // tile.  All sixteen key fragments are read from LDS first, then the
-        // MFMAs run k-step-major over the four accumulators, so that no MFMA
-        // waits for an LDS round trip or for the one before it in its chain
-        // (read, wait, two dependent MFMAs per fragment made the tile a chain of
-        // LDS latencies).  Each accumulator still sums hi, lo of k-step 0, then
-        // of k-step 1, ...
+        // tile.  The key fragments are read from LDS first, then the MFMAs run
+        // k-step-major over the accumulators, so that no MFMA waits for an LDS
+        // round trip or for the one before it in its chain (read, wait, two
+        // dependent MFMAs per fragment made the tile a chain of LDS latencies).
+        // With two pairs per wavefront the registers hold one column tile's
+        // four fragments at a time (more would spill: the two pairs' Q fragments and
+        // output accumulators take 128 registers).  Each accumulator still sums
+        // hi, lo of k-step 0, then of k-step 1, ...
+        constexpr int NTH = PPW == 1 ? 4 : 1;  // key fragments' column tiles held at once
         f32x4 s[PPW][4];
-        bf16x8 kb[4][4];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kb[nt][ks] = ld16(&Kt[(nt * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
 #pragma unroll
         for (int i = 0; i < PPW; ++i)
 #pragma unroll
             for (int nt = 0; nt < 4; ++nt) s[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+        for (int n0 = 0; n0 < 4; n0 += NTH) {
+            bf16x8 kb[NTH][4];
 #pragma unroll
-            for (int i = 0; i < PPW; ++i) {
-                if (!pvalid[i]) continue;
+            for (int nt = 0; nt < NTH; ++nt)
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt)
-                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], qv[i][ks], s[i][nt], 0, 0, 0);
+                for (int ks = 0; ks < 4; ++ks)
+                    kb[nt][ks] = ld16(&Kt[((n0 + nt) * 16 + (lane & 15)) * KS_STRIDE + ks * 32 + 8 * g]);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt)
-                    s[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], ql[i][ks], s[i][nt], 0, 0, 0);
-            }
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int i = 0; i < PPW; ++i) {
+                    if (!pvalid[i]) continue;
+#pragma unroll
+                    for (int nt = 0; nt < NTH; ++nt)
+                        s[i][n0 + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], qv[i][ks], s[i][n0 + nt], 0, 0, 0);
+#pragma unroll
+                    for (int nt = 0; nt < NTH; ++nt)
+                        s[i][n0 + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[nt][ks], ql[i][ks], s[i][n0 + nt], 0, 0, 0);
+                }
+        }
         // online softmax, one query row per lane column
         bf16x8 pb[PPW][2], pl[PPW][2];
 #pragma unroll
@@ -262,33 +269,41 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(const bf16_t
             }
         }
         // O^T += V^T P^T: A operand = V^T rows (dims 16*nt + lane%16) over the
-        // same key slots; as above, every fragment is read first and the MFMAs
-        // of the eight accumulators then interleave (same per-accumulator order)
-        bf16x8 va[8][2];
+        // same key slots; as above, the fragments are read first (half of them
+        // at a time with two pairs per wavefront, for the same reason) and the MFMAs of the
+        // accumulators then interleave (same per-accumulator order)
+        constexpr int NVH = PPW == 1 ? 8 : 4;  // value fragments' column tiles held at once
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt)
+        for (int n0 = 0; n0 < 8; n0 += NVH) {
+            bf16x8 va[NVH][2];
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                // this lane addresses key ks*32 + 4g + m (then + 16), dims
-                // 16 nt + 4q .. +3, for m = (lane%16)/4, q = lane%4; it receives
-                // dim 16 nt + lane%16 of keys ks*32 + 4g + 0..3 and + 16 + 0..3
-                const bf16_t *vr = &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * VS_STRIDE + nt * 16 + 4 * (lane & 3)];
-                const i16x4 lo = lds_read_tr16(vr);
-                const i16x4 hi = lds_read_tr16(vr + 16 * VS_STRIDE);
-                va[nt][ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            }
+            for (int nt = 0; nt < NVH; ++nt)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+                for (int ks = 0; ks < 2; ++ks) {
+                    // this lane addresses key ks*32 + 4g + m (then + 16), dims
+                    // 16 nt + 4q .. +3, for m = (lane%16)/4, q = lane%4; it receives
+                    // dim 16 nt + lane%16 of keys ks*32 + 4g + 0..3 and + 16 + 0..3
+                    const bf16_t *vr =
+                        &Vt[(ks * 32 + 4 * g + ((lane & 15) >> 2)) * VS_STRIDE + (n0 + nt) * 16 + 4 * (lane & 3)];
+                    const i16x4 lo = lds_read_tr16(vr);
+                    const i16x4 hi = lds_read_tr16(vr + 16 * VS_STRIDE);
+                    va[nt][ks] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                }
 #pragma unroll
-            for (int i = 0; i < PPW; ++i) {
-                if (!pvalid[i]) continue;
+            for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-                for (int nt = 0; nt < 8; ++nt)
-                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pb[i][ks], oacc[i][nt], 0, 0, 0);
+                for (int i = 0; i < PPW; ++i) {
+                    if (!pvalid[i]) continue;
 #pragma unroll
-                for (int nt = 0; nt < 8; ++nt)
-                    oacc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pl[i][ks], oacc[i][nt], 0, 0, 0);
-            }
+                    for (int nt = 0; nt < NVH; ++nt)
+                        oacc[i][n0 + nt] =
+                            __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pb[i][ks], oacc[i][n0 + nt], 0, 0, 0);
+#pragma unroll
+                    for (int nt = 0; nt < NVH; ++nt)
+                        oacc[i][n0 + nt] =
+                            __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[nt][ks], pl[i][ks], oacc[i][n0 + nt], 0, 0, 0);
+                }
+        }
     }
 #undef KVR_ATT_FETCH
 
