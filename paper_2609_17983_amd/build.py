@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(os.path.dirname(PKG), "_build")
 LIB = os.path.join(PKG, "libkvr.so")
 
-SOURCES = ["engine.hip", "kernels_basic.hip", "gemm_skinny.hip", "gemm_tiled.hip", "attention.hip", "pack.hip",
+SOURCES = ["engine.hip", "kernels_basic.hip", "gemm_skinny.hip", "gemm_tiled.hip", "gemm_tall.hip", "attention.hip", "pack.hip",
            "scoring.hip", "select_gpu.hip", "select.cpp", "metrics.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -134,6 +134,7 @@ struct LinearArgs {
     int32_t split;        // tiled STORE only: K cut into `split` slices, partial
                           // tiles out[s][R][ldo] summed by the consumer (<= 1: none)
     int32_t group_all;    // tiled: at most this many row blocks form one group of the tile order (set by the launcher)
+    int32_t tpb;          // tall kernel: weight tiles per block (0: not the tall kernel)
 };
 
 // Skinny (R <= 64) linear layer: X in operand order, W packed in operand order
@@ -219,6 +220,16 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
 // Tiled MFMA path for many rows (packed weight, K a multiple of 32,
 // activations in operand order).
 hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
+// Tall MFMA path for 64 < R <= 16 * TALL_MT_MAX rows (packed weight,
+// activations in operand order): a block holds every row; a.tpb weight tiles
+// per block and a.split K slices come from plan_tall.
+constexpr int TALL_MT_MAX = 12;    // 16-row tiles a block holds (its activation ring: four stages of 2 MT KB)
+constexpr int TALL_TPB = 12;       // weight tiles per block at most (three per wavefront)
+constexpr int TALL_SPLIT_MAX = 32;
+struct TallPlan { int tpb, split; };
+bool tall_rows_ok(int R);
+TallPlan plan_tall(int R, int vrows, int K, bool swiglu, size_t p_floats);
+hipError_t launch_linear_tall(int epi, const LinearArgs &a, hipStream_t s);
 // Output-tile blocks the tiled kernel launches for R rows and vrows weight
 // rows (before any K split), and how many of them the chip runs at once.
 int tiled_blocks(int R, int vrows, int *slots);

@@ -329,6 +329,7 @@ bool skinny_pass_ok(const kvr_ctx *c, int R) { return c->wpk != nullptr && R <= 
 // Packed weight: the tiled MFMA kernel, whose activations are in operand
 // order; otherwise the row-major simple kernel.
 hipError_t linear(kvr_ctx *c, int epi, LinearArgs a, hipStream_t s) {
+    if (a.wp && a.tpb > 0) return launch_linear_tall(epi, a, s);
     if (a.wp) return launch_linear_tiled(epi, a, s);
     return launch_linear_simple(c->bf16, epi, a, s);
 }
@@ -376,6 +377,28 @@ int tiled_split(const kvr_ctx *c, int R, int vrows, int K) {
     split = std::min(split, std::max(1, K / 32 / 16));
     split = std::min<long long>(split, (long long)(c->p_floats / ((size_t)R * vrows)));
     return std::max(1, std::min(split, SPLIT_MAX));
+}
+
+// Kernel and K split of a packed-weight projection outside skinny passes: the
+// tall kernel for 64 < R <= 192 rows (KVR_TALL=0 turns it off; KVR_TALL_TPB
+// and KVR_TALL_SPLIT force its plan), the tiled kernel otherwise (split for
+// STORE projections only).
+void plan_packed(const kvr_ctx *c, LinearArgs &a, int epi) {
+    const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+    a.tpb = 0;
+    a.split = 1;
+    if (!a.wp) return;
+    if (tall_rows_ok(a.R) && env_int("KVR_TALL", 1) != 0) {
+        TallPlan p = plan_tall(a.R, vrows, a.K, epi == EPI_SWIGLU, c->p_floats);
+        const int tpb = env_int("KVR_TALL_TPB", 0), sp = env_int("KVR_TALL_SPLIT", 0);
+        if (tpb >= 1 && tpb <= TALL_TPB) p.tpb = tpb;
+        if (sp >= 1 && epi == EPI_STORE && (size_t)sp * a.R * vrows <= c->p_floats)
+            p.split = std::min(sp, std::min(TALL_SPLIT_MAX, a.K / 32));
+        a.tpb = p.tpb;
+        a.split = p.split;
+        return;
+    }
+    if (epi == EPI_STORE) a.split = tiled_split(c, a.R, vrows, a.K);
 }
 
 // Step profiler: arm() hands two events to the next kernel launch, which
@@ -505,7 +528,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             LinearArgs a = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr,
                                      NQKV);
             a.grp = c->qkv_grp;
-            if (pw.qkv) a.split = tiled_split(c, R, NQKV, D);
+            plan_packed(c, a, EPI_STORE);
             KVR_CHECK(linear(c, EPI_STORE, a, s), "qkv", ST_QKV);
             qkv_split = a.split;
         }
@@ -539,7 +562,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             // packed: partial tiles into P (the next RMSNorm adds them to H)
             LinearArgs a = make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->P, nullptr, D);
             a.grp = c->o_grp;
-            a.split = tiled_split(c, R, D, qd);
+            plan_packed(c, a, EPI_STORE);
             KVR_CHECK(linear(c, EPI_STORE, a, s), "o_proj", ST_OPROJ);
             resid_split = a.split;
         } else {
@@ -565,12 +588,13 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             LinearArgs ga = make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu, c->Ab,
                                       c->Ab_lo, F);
             ga.grp = c->gu_grp;
+            plan_packed(c, ga, EPI_SWIGLU);
             KVR_CHECK(linear(c, EPI_SWIGLU, ga, s), "gate_up", ST_GATEUP);
             if (pw.down) {
                 LinearArgs a = make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down, c->P,
                                          nullptr, D);
                 a.grp = c->down_grp;
-                a.split = tiled_split(c, R, D, F);
+                plan_packed(c, a, EPI_STORE);
                 KVR_CHECK(linear(c, EPI_STORE, a, s), "down", ST_DOWN);
                 resid_split = a.split;
             } else {

@@ -450,6 +450,58 @@ def test_mid_attention_plan_overrides(mid, monkeypatch, env):
     _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid EditLocal K=32, attention plan {env}")
 
 
+# Passes of 65-192 rows run the tall kernel (a block holds every row): one
+# repair per row-tile count 5-12, with the plans the planner picks.
+TALL_ROWS = [(66, "edit_local"), (95, "random"), (100, "edit_local"), (128, "random"), (129, "edit_local"),
+             (150, "random"), (170, "edit_local"), (192, "random")]
+
+
+@pytest.mark.parametrize("rows,policy", TALL_ROWS, ids=[f"{r}-{p}" for r, p in TALL_ROWS])
+def test_mid_tall_rows(mid, rows, policy):
+    shape, eng, ow, toks, new, stale_np = mid
+    K = rows - 16
+    A = (osel.select_edit_local(700, 300, 316, K) if policy == "edit_local"
+         else osel.select_random(700, 300, 316, K, rows))
+    _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid {policy} K={K} ({rows} rows, tall kernel)",
+                 n_cap=704)
+
+
+# Tall plans forced through the overrides: tiles per block that leave some
+# wavefronts with fewer tiles (or none), K splits of every STORE projection
+# that do not divide its k-steps, and the tiled kernel for the same rows.
+TALL_OVERRIDES = [{"KVR_TALL_TPB": "5", "KVR_TALL_SPLIT": "3"}, {"KVR_TALL_TPB": "1", "KVR_TALL_SPLIT": "7"},
+                  {"KVR_TALL_TPB": "12", "KVR_TALL_SPLIT": "1"}, {"KVR_TALL": "0"}]
+
+
+@pytest.mark.parametrize("env", TALL_OVERRIDES, ids=["tpb5-split3", "tpb1-split7", "tpb12-unsplit", "tiled"])
+def test_mid_tall_plan_overrides(mid, monkeypatch, env):
+    shape, eng, ow, toks, new, stale_np = mid
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    A = osel.select_random(700, 300, 316, 128, 5)
+    _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid Random K=128, tall plan {env}", n_cap=704)
+
+
+def test_mid_short_prefill_tall():
+    """A 150-token prefill: every projection of the pass on the tall kernel."""
+    shape, n = MID, 150
+    eng, ow, toks = _setup(shape, kvr.KVR_BF16, n, n, seed=21)
+    try:
+        say(f"case: {shape.name} prefill n={n} (tall kernel)")
+        cache = eng.new_cache(n)
+        hidden = torch.empty((n, shape.d_model), device="cuda")
+        eng.prefill(toks.cuda(), cache, hidden)
+        torch.cuda.synchronize()
+        oc, oy = od.prefill(shape, ow, toks.numpy())
+        got = cache.to(torch.float64).cpu().numpy()
+        errs = {(l, kv): relmax(got[l, kv], oc[l, kv]) for l in range(shape.n_layers) for kv in range(2)}
+        errs["hidden"] = relmax(hidden.cpu().numpy(), oy)
+        say(f"  {errs}")
+        assert max(errs.values()) <= TOL[kvr.KVR_BF16]
+    finally:
+        eng.close()
+
+
 @pytest.mark.parametrize("nt", ["2", "5"])
 def test_ragged_gateup_blocks_across_groups(monkeypatch, nt):
     """Gate/up packed in groups of three tiles, read by blocks of two or five
