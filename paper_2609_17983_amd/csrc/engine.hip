@@ -210,7 +210,8 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
             }
         }
     };
-    const int target = env_int("KVR_ATT_TARGET", 256);
+    const int target_env = env_int("KVR_ATT_TARGET", 0);
+    int target = target_env > 0 ? target_env : 256;
     const int mt_max = attention_max_row_tiles(c->d.n_heads, Hkv);
     int mt = mt_max;
     make_blocks(16 * mt);
@@ -233,6 +234,15 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
     const size_t max_slots = c->attn_part_floats / slot_floats;
     if (split) {
         long long ks = (total_keys * Hkv + target - 1) / target;
+        // Items of a dozen key tiles or more (many rows: Qwen2.5-7B shape at
+        // 528 rows, 17-tile items) run as twice as many half-length items:
+        // the units that finish early take the rest, and the last round is
+        // short (attention 59.5 -> 48.0 us per layer; at 144 rows, 5-tile
+        // items, the doubled target cost 17.1 -> 23.0 us)
+        if (target_env <= 0 && ks >= 12 * ATT_KT) {
+            target *= 2;
+            ks = (total_keys * Hkv + target - 1) / target;
+        }
         ks = std::max<long long>(env_int("KVR_ATT_MINKS", 128), (ks + ATT_KT - 1) / ATT_KT * ATT_KT);
         for (;; ks *= 2) {
             size_t slots = 0, nitems = 0;
