@@ -225,11 +225,22 @@ hipError_t launch_linear_tiled(int epi, const LinearArgs &a, hipStream_t s);
 // per block and a.split K slices come from plan_tall.
 constexpr int TALL_MT_MAX = 12;    // 16-row tiles a block holds (its activation ring: four stages of 2 MT KB)
 constexpr int TALL_TPB = 12;       // weight tiles per block at most (three per wavefront)
+constexpr int TALL_TPB_WIDE = 20;  // ... for STORE launches (five per wavefront)
 constexpr int TALL_SPLIT_MAX = 32;
+constexpr int TALL_GU_SPLIT_MAX = 2;  // K slices of a split gate/up projection
+// tpb weight tiles per block, split K slices.  For the SwiGLU projection a
+// split > 1 means: the gate/up columns go to fp32 partial tiles (a STORE
+// launch over 2 N virtual columns) and launch_swiglu_partials finishes them.
 struct TallPlan { int tpb, split; };
 bool tall_rows_ok(int R);
-TallPlan plan_tall(int R, int vrows, int K, bool swiglu, size_t p_floats);
+// store_tpb_max: widest block a STORE plan may take (TALL_TPB .. TALL_TPB_WIDE)
+TallPlan plan_tall(int R, int vrows, int K, bool swiglu, size_t p_floats, int store_tpb_max);
 hipError_t launch_linear_tall(int epi, const LinearArgs &a, hipStream_t s);
+// A[r][f] = silu(g) * u with g, u the sums over `nsplit` fp32 partial tiles
+// part[s][R][2F] of the gate/up-interleaved columns (column 16t + j: gate of
+// feature 8t + j for j < 8, up of feature 8t + j - 8 otherwise); A is written
+// as a compensated pair in operand order ([R][F], F a multiple of 32).
+hipError_t launch_swiglu_partials(const float *part, int nsplit, int R, int F, bf16_t *A, bf16_t *A_lo, hipStream_t s);
 // Output-tile blocks the tiled kernel launches for R rows and vrows weight
 // rows (before any K split), and how many of them the chip runs at once.
 int tiled_blocks(int R, int vrows, int *slots);

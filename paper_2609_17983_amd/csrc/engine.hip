@@ -133,11 +133,11 @@ constexpr int SPLIT_MAX = 32;
 
 enum Step {
     ST_EMBED, ST_NORM, ST_QKV, ST_ROPE, ST_ATTN, ST_COMBINE, ST_OPROJ, ST_GATEUP, ST_DOWN, ST_FINAL, ST_LMHEAD,
-    ST_LOGSOFTMAX, ST_MASS, ST_COUNT
+    ST_LOGSOFTMAX, ST_MASS, ST_SWIGLU, ST_COUNT
 };
 const char *const STEP_NAMES[ST_COUNT] = {"embed", "rmsnorm", "qkv_proj", "rope_scatter", "attention",
                                           "attention_combine", "o_proj", "gate_up_swiglu", "down_proj", "final_norm",
-                                          "lm_head", "logsoftmax", "attention_mass"};
+                                          "lm_head", "logsoftmax", "attention_mass", "swiglu_partials"};
 constexpr int SCORE_ROWS = 64;  // rows per LM-head launch (the skinny kernel's bound)
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -390,19 +390,30 @@ int tiled_split(const kvr_ctx *c, int R, int vrows, int K) {
 }
 
 // Kernel and K split of a packed-weight projection outside skinny passes: the
-// tall kernel for 64 < R <= 192 rows (KVR_TALL=0 turns it off; KVR_TALL_TPB
-// and KVR_TALL_SPLIT force its plan), the tiled kernel otherwise (split for
-// STORE projections only).
+// tall kernel for 64 < R <= 192 rows, the tiled kernel otherwise (split for
+// STORE projections only).  A tall SwiGLU plan with split > 1 runs as a STORE
+// launch into P followed by the SwiGLU pass (run_pass).  Environment
+// overrides of the tall plan: KVR_TALL=0 (tiled kernel instead),
+// KVR_TALL_TPB (tiles per block), KVR_TALL_SPLIT (STORE split),
+// KVR_TALL_GU_SPLIT (SwiGLU split, 1 or 2), KVR_TALL_STORE_TPB (widest STORE
+// block the planner may take, 12-20).
 void plan_packed(const kvr_ctx *c, LinearArgs &a, int epi) {
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
     a.tpb = 0;
     a.split = 1;
     if (!a.wp) return;
     if (tall_rows_ok(a.R) && env_int("KVR_TALL", 1) != 0) {
-        TallPlan p = plan_tall(a.R, vrows, a.K, epi == EPI_SWIGLU, c->p_floats);
+        const bool gu = epi == EPI_SWIGLU;
+        const int store_max = std::min(TALL_TPB_WIDE, std::max(TALL_TPB, env_int("KVR_TALL_STORE_TPB", TALL_TPB)));
+        TallPlan p = plan_tall(a.R, vrows, a.K, gu, c->p_floats, store_max);
+        const int gsp = gu ? env_int("KVR_TALL_GU_SPLIT", 0) : 0;
+        if (gsp >= 1 && gsp <= TALL_GU_SPLIT_MAX && (size_t)gsp * a.R * vrows <= c->p_floats) {
+            p.split = gsp;
+            p.tpb = std::max(1, std::min(gsp == 1 ? TALL_TPB : TALL_TPB_WIDE, (vrows / 16 * gsp + 255) / 256));
+        }
         const int tpb = env_int("KVR_TALL_TPB", 0), sp = env_int("KVR_TALL_SPLIT", 0);
-        if (tpb >= 1 && tpb <= TALL_TPB) p.tpb = tpb;
-        if (sp >= 1 && epi == EPI_STORE && (size_t)sp * a.R * vrows <= c->p_floats)
+        if (tpb >= 1 && tpb <= ((gu && p.split == 1) ? TALL_TPB : TALL_TPB_WIDE)) p.tpb = tpb;
+        if (sp >= 1 && !gu && (size_t)sp * a.R * vrows <= c->p_floats)
             p.split = std::min(sp, std::min(TALL_SPLIT_MAX, a.K / 32));
         a.tpb = p.tpb;
         a.split = p.split;
@@ -599,7 +610,22 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                                       c->Ab_lo, F);
             ga.grp = c->gu_grp;
             plan_packed(c, ga, EPI_SWIGLU);
-            KVR_CHECK(linear(c, EPI_SWIGLU, ga, s), "gate_up", ST_GATEUP);
+            if (ga.tpb > 0 && ga.split > 1) {
+                // split gate/up (tall): fp32 partials of the 2F interleaved
+                // columns into P (free: the residual step consumed the output
+                // projection's), then the SwiGLU pass writes the down
+                // projection's operand
+                LinearArgs pa = ga;
+                pa.N = 2 * F;
+                pa.out = c->P;
+                pa.out_lo = nullptr;
+                pa.ldo = 2 * F;
+                KVR_CHECK(launch_linear_tall(EPI_STORE, pa, s), "gate_up", ST_GATEUP);
+                KVR_CHECK(launch_swiglu_partials(c->P, ga.split, R, F, (bf16_t *)c->Ab, (bf16_t *)c->Ab_lo, s),
+                          "swiglu_partials", ST_SWIGLU);
+            } else {
+                KVR_CHECK(linear(c, EPI_SWIGLU, ga, s), "gate_up", ST_GATEUP);
+            }
             if (pw.down) {
                 LinearArgs a = make_args(c->Ab, c->Ab_lo, F, R, F, D, w.w_down, w.w_down, w.w_down, D, D, pw.down, c->P,
                                          nullptr, D);
@@ -786,7 +812,10 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
     const size_t R = align_up((size_t)c->rows_cap, 64);
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
-    const size_t p_floats = std::max(R * (qd + 2 * kd), (size_t)SPLIT_MAX * 64 * std::max(qd + 2 * kd, D));
+    // P also takes a split tall gate/up projection's partials (passes of 65-192 rows)
+    const size_t tall_rows = c->rows_cap > 64 ? std::min<size_t>(R, 16 * TALL_MT_MAX) : 0;
+    const size_t p_floats = std::max({R * (qd + 2 * kd), (size_t)SPLIT_MAX * 64 * std::max(qd + 2 * kd, D),
+                                      (size_t)TALL_GU_SPLIT_MAX * tall_rows * 2 * F});
     const size_t lo_es = c->bf16 ? es : 0;  // compensated low parts exist in bf16 only
     const size_t o_H = take(R * D * 4), o_P = take(p_floats * 4), o_Xn = take(R * D * es),
                  o_Qb = take(R * qd * es), o_Ob = take(R * qd * es), o_Ab = take(R * F * es),

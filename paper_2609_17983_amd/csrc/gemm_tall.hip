@@ -11,14 +11,15 @@
 // gives a block every row of the pass: each weight element is read from HBM
 // once and multiplies all rows.
 //
-// A block owns up to TALL_TPB consecutive 16-row weight tiles and one of
-// `split` slices of K.  Per k-step, the 2 MT activation fragments (hi and lo
+// A block owns up to TALL_TPB (STORE launches: TALL_TPB_WIDE) consecutive
+// 16-row weight tiles and one of `split` slices of K.  Per k-step, the 2 MT activation fragments (hi and lo
 // of every 16-row tile) and the block's weight fragments are copied straight
 // from memory into a ring of LDS stages (global_load_lds_dwordx4; both
 // operands are stored in operand order, so each 16 x 32 fragment is one
 // contiguous 1 KB block, and lane l's 16 bytes land at byte 16 l), STAGES - 1
-// k-steps ahead.  The four wavefronts share the activation fragments;
-// wavefront w owns the block's weight tiles w, w + 4, w + 8 and keeps their
+// k-steps ahead (three, or two where four stages do not fit in LDS).  The
+// four wavefronts share the activation fragments; wavefront w owns the
+// block's weight tiles w, w + 4, w + 8 (, w + 12, w + 16) and keeps their
 // accumulators for all rows, so no reduction across wavefronts is needed.
 // Each wavefront copies the same number of fragments per k-step (the short
 // ones repeat their last fragment), so the count of its loads in flight is
@@ -28,15 +29,19 @@
 // What bounds it: a compute unit takes in about 30 GB/s of this mix of
 // weight (HBM) and activation (L2) fragments, so a projection costs its bytes
 // per unit at that rate.  A K split cuts each unit's share of the activation
-// matrix; the SwiGLU projection is never split, and at 144 rows its 2 MB of
-// compensated activations per unit (beside 1 MB of weights) hold it at the
-// tiled kernel's time.  Measured and rejected: a fifth stage (four k-steps in
+// matrix.  The SwiGLU projection needs whole dot products: unsplit it runs
+// with the SwiGLU in the epilogue, and at 144 rows its 2 MB of compensated
+// activations per unit (beside 1 MB of weights) hold it at the tiled
+// kernel's time; split in two it runs as a STORE launch of up to twenty
+// tiles per block (1 MB of activations per unit) into fp32 partials that
+// swiglu_partials_kernel sums, activates and writes as the down projection's
+// operand.  Measured and rejected: a fifth stage (four k-steps in
 // flight; Qwen2.5-7B shape, 144 rows: 6.93 against 6.80 ms per repair), and
 // wavefronts 0-1 copying the activations with 2-3 copying the weights into a
 // twice deeper ring (every projection about twice slower).
 //
 // Outputs as the tiled kernel: STORE writes fp32 partial tiles [split][R][ldo]
-// that the next row-wise kernel sums in a fixed order; SWIGLU (never split)
+// that the next row-wise kernel sums in a fixed order; SWIGLU (unsplit)
 // takes gate/up-interleaved tiles and writes silu(gate) * up in operand order.
 #include <algorithm>
 
@@ -46,10 +51,12 @@ namespace kvr {
 
 namespace {
 
-constexpr int TPB = TALL_TPB;       // weight tiles per block at most
-constexpr int NTW = TPB / 4;        // weight tiles per wavefront at most
 constexpr int FRAG = 512;           // bf16 elements per fragment (1 KB)
-constexpr int STAGES = 4;          // LDS ring stages: three k-steps in flight
+
+// LDS ring stages for MT activation tiles and TPB weight tiles per k-step:
+// four (three k-steps in flight) where they fit in 160 KB, else three.
+template <int MT, int TPB>
+constexpr int tall_stages() { return 4 * (2 * MT + TPB) * FRAG * 2 <= 160 * 1024 ? 4 : 3; }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
 
@@ -84,8 +91,10 @@ __device__ __forceinline__ void wait_later(int later) {
     }
 }
 
-template <int MT, int EPI>
+template <int MT, int TPB, int EPI>
 __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
+    constexpr int NTW = TPB / 4;        // weight tiles per wavefront at most
+    constexpr int STAGES = tall_stages<MT, TPB>();
     constexpr int NX = 2 * MT;          // activation fragments per k-step: hi row tiles, then lo
     constexpr int NF = NX + TPB;        // fragments per k-step in a stage
     constexpr int FPW = (NF + 3) / 4;   // fragments each wavefront copies per k-step
@@ -210,36 +219,85 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
 
 template <int MT>
 hipError_t launch_mt(int epi, const LinearArgs &a, int blocks, hipStream_t s) {
-    if (epi == EPI_SWIGLU) kvr_launch((linear_tall_kernel<MT, EPI_SWIGLU>), dim3(blocks), dim3(256), 0, s, a);
-    else kvr_launch((linear_tall_kernel<MT, EPI_STORE>), dim3(blocks), dim3(256), 0, s, a);
+    if (epi == EPI_SWIGLU) kvr_launch((linear_tall_kernel<MT, TALL_TPB, EPI_SWIGLU>), dim3(blocks), dim3(256), 0, s, a);
+    else if (a.tpb <= TALL_TPB) kvr_launch((linear_tall_kernel<MT, TALL_TPB, EPI_STORE>), dim3(blocks), dim3(256), 0, s, a);
+    else kvr_launch((linear_tall_kernel<MT, TALL_TPB_WIDE, EPI_STORE>), dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+// One thread per (row, eight features): the gate and up partials of the
+// features' weight tile summed in split order, SwiGLU, and one 16-byte store
+// each of the hi and lo parts (eight consecutive features are contiguous in
+// operand order).
+__global__ __launch_bounds__(256) void swiglu_partials_kernel(const float *part, int nsplit, int R, int F, bf16_t *A,
+                                                               bf16_t *A_lo) {
+    const int per_row = F >> 3;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= R * per_row) return;
+    const int r = idx / per_row, t = idx - r * per_row;
+    const size_t row = (size_t)2 * F;
+    const float *p = part + (size_t)r * row + 16 * t;
+    f32x4 g0 = *reinterpret_cast<const f32x4 *>(p), g1 = *reinterpret_cast<const f32x4 *>(p + 4);
+    f32x4 u0 = *reinterpret_cast<const f32x4 *>(p + 8), u1 = *reinterpret_cast<const f32x4 *>(p + 12);
+    for (int q = 1; q < nsplit; ++q) {
+        const float *pq = p + (size_t)q * R * row;
+        g0 += *reinterpret_cast<const f32x4 *>(pq);
+        g1 += *reinterpret_cast<const f32x4 *>(pq + 4);
+        u0 += *reinterpret_cast<const f32x4 *>(pq + 8);
+        u1 += *reinterpret_cast<const f32x4 *>(pq + 12);
+    }
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        y[e] = silu_f(g0[e]) * u0[e];
+        y[4 + e] = silu_f(g1[e]) * u1[e];
+    }
+    uint32_t hi[4], lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const bf16_t h0 = f32_to_bf16(y[2 * e]), h1 = f32_to_bf16(y[2 * e + 1]);
+        const bf16_t l0 = f32_to_bf16(y[2 * e] - bf16_to_f32(h0)), l1 = f32_to_bf16(y[2 * e + 1] - bf16_to_f32(h1));
+        hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        lo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    }
+    const size_t off = perm_offset(r, 8 * t, F);
+    *reinterpret_cast<u32x4 *>(A + off) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+    *reinterpret_cast<u32x4 *>(A_lo + off) = u32x4{lo[0], lo[1], lo[2], lo[3]};
 }
 
 }  // namespace
 
 bool tall_rows_ok(int R) { return R > 64 && R <= 16 * TALL_MT_MAX; }
 
-// Weight tiles per block and K split.  SwiGLU is never split: the tiles are
-// dealt evenly to at most 256 blocks.  A STORE projection takes the split
-// (and the fewest tiles per block that keep the grid within 256 blocks) that
-// minimises the bytes one block reads and writes: activations R x K/split x
-// 4 bytes (a compensated pair), weights tiles x 16 x K/split x 2 bytes and its
-// partial tile; the partial buffer bounds the split.  With more than 256 x
-// TALL_TPB tiles the grid takes several rounds of full blocks.
-TallPlan plan_tall(int R, int vrows, int K, bool swiglu, size_t p_floats) {
+// Weight tiles per block and K split: the plan (tiles per block that keep
+// the grid within 256 blocks for each split) that minimises the bytes one
+// block reads and writes: activations R x K/split x 4 bytes (a compensated
+// pair), weights tiles x 16 x K/split x 2 bytes and, when split, its fp32
+// partial tile; the partial buffer bounds the split.  A STORE projection
+// takes blocks of up to store_tpb_max tiles and splits up to TALL_SPLIT_MAX.
+// The SwiGLU projection runs unsplit (at most TALL_TPB tiles per block, the
+// SwiGLU in the epilogue) or, split in two, as a STORE launch of up to
+// TALL_TPB_WIDE tiles per block whose partials the SwiGLU pass finishes; its
+// cost adds that pass's reads and writes spread over 256 compute units.  At
+// 144 rows (Qwen2.5-7B shape) the unsplit block takes in 2 MB of
+// activations beside its 1 MB of weights, the split one half of that.  With
+// more than 256 x TALL_TPB tiles the grid takes several rounds of full blocks.
+TallPlan plan_tall(int R, int vrows, int K, bool swiglu, size_t p_floats, int store_tpb_max) {
     const int ntiles = vrows / 16, ksteps = K / 32;
     const long long rows = (R + 15) / 16 * 16;
-    TallPlan p{std::min(TPB, std::max(1, (ntiles + 255) / 256)), 1};
-    if (swiglu) return p;
+    TallPlan p{std::min(TALL_TPB, std::max(1, (ntiles + 255) / 256)), 1};
+    const int spmax = swiglu ? TALL_GU_SPLIT_MAX : TALL_SPLIT_MAX;
     long long best = -1;
-    for (int sp = 1; sp <= std::min(TALL_SPLIT_MAX, std::max(1, ksteps / 4)); ++sp) {
+    for (int sp = 1; sp <= std::min(spmax, std::max(1, ksteps / 4)); ++sp) {
         if (sp > 1 && (size_t)sp * R * vrows > p_floats) break;
         const int cols = 256 / sp;
         if (cols < 1) break;
         const int tpb = (ntiles + cols - 1) / cols;
-        if (tpb > TPB) continue;
+        const int cap = swiglu ? (sp == 1 ? TALL_TPB : TALL_TPB_WIDE) : store_tpb_max;
+        if (tpb > cap) continue;
         const long long ks = (ksteps + sp - 1) / sp;
-        const long long bytes = ks * 32 * (rows * 4 + (long long)tpb * 16 * 2) + (sp > 1 ? rows * tpb * 16 * 4 : 0);
+        long long bytes = ks * 32 * (rows * 4 + (long long)tpb * 16 * 2) + (sp > 1 ? rows * tpb * 16 * 4 : 0);
+        if (swiglu && sp > 1) bytes += ((long long)sp * R * vrows * 4 + (long long)R * (vrows / 2) * 4) / 256;
         if (best < 0 || bytes < best) {
             best = bytes;
             p = TallPlan{tpb, sp};
@@ -253,7 +311,9 @@ hipError_t launch_linear_tall(int epi, const LinearArgs &a, hipStream_t s) {
     if (!tall_rows_ok(a.R) || !a.x_lo || !a.wp || (epi == EPI_SWIGLU && !a.out_lo)) return hipErrorInvalidValue;
     if (epi != EPI_STORE && epi != EPI_SWIGLU) return hipErrorInvalidValue;
     const int vrows = epi == EPI_SWIGLU ? 2 * a.N : a.N;
-    if (a.K % 32 != 0 || a.K < 32 || vrows % 16 != 0 || a.tpb < 1 || a.tpb > TPB) return hipErrorInvalidValue;
+    if (a.K % 32 != 0 || a.K < 32 || vrows % 16 != 0 || a.tpb < 1 ||
+        a.tpb > (epi == EPI_SWIGLU ? TALL_TPB : TALL_TPB_WIDE))
+        return hipErrorInvalidValue;
     const int split = a.split > 1 ? a.split : 1;
     if (split > a.K / 32 || (epi == EPI_SWIGLU && split != 1)) return hipErrorInvalidValue;
     const int blocks = (vrows / 16 + a.tpb - 1) / a.tpb * split;
@@ -267,6 +327,16 @@ hipError_t launch_linear_tall(int epi, const LinearArgs &a, hipStream_t s) {
         case 11: return launch_mt<11>(epi, a, blocks, s);
         default: return launch_mt<12>(epi, a, blocks, s);
     }
+}
+
+hipError_t launch_swiglu_partials(const float *part, int nsplit, int R, int F, bf16_t *A, bf16_t *A_lo,
+                                  hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    if (!part || !A || !A_lo || nsplit < 1 || F % 32 != 0) return hipErrorInvalidValue;
+    const long long items = (long long)R * (F / 8);
+    kvr_launch(swiglu_partials_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, part, nsplit, R, F, A,
+               A_lo);
+    return hipGetLastError();
 }
 
 }  // namespace kvr
