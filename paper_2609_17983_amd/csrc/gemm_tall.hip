@@ -228,13 +228,16 @@ hipError_t launch_mt(int epi, const LinearArgs &a, int blocks, hipStream_t s) {
 // One thread per (row, eight features): the gate and up partials of the
 // features' weight tile summed in split order, SwiGLU, and one 16-byte store
 // each of the hi and lo parts (eight consecutive features are contiguous in
-// operand order).
+// operand order).  The 16 rows of a row tile are the fastest index, so that
+// 16 neighbouring threads store 256 contiguous bytes of an operand fragment.
 __global__ __launch_bounds__(256) void swiglu_partials_kernel(const float *part, int nsplit, int R, int F, bf16_t *A,
                                                                bf16_t *A_lo) {
     const int per_row = F >> 3;
     const int idx = blockIdx.x * 256 + threadIdx.x;
-    if (idx >= R * per_row) return;
-    const int r = idx / per_row, t = idx - r * per_row;
+    const int q = idx >> 4;
+    const int rt = q / per_row, t = q - rt * per_row;
+    const int r = rt * 16 + (idx & 15);
+    if (r >= R) return;
     const size_t row = (size_t)2 * F;
     const float *p = part + (size_t)r * row + 16 * t;
     f32x4 g0 = *reinterpret_cast<const f32x4 *>(p), g1 = *reinterpret_cast<const f32x4 *>(p + 4);
@@ -333,7 +336,7 @@ hipError_t launch_swiglu_partials(const float *part, int nsplit, int R, int F, b
                                   hipStream_t s) {
     if (R <= 0) return hipSuccess;
     if (!part || !A || !A_lo || nsplit < 1 || F % 32 != 0) return hipErrorInvalidValue;
-    const long long items = (long long)R * (F / 8);
+    const long long items = (long long)((R + 15) / 16 * 16) * (F / 8);
     kvr_launch(swiglu_partials_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, part, nsplit, R, F, A,
                A_lo);
     return hipGetLastError();

@@ -190,46 +190,94 @@ __global__ __launch_bounds__(64 * TileShape<RT>::NW, TileShape<RT>::BLOCKS_PER_C
             }
     }
 
-    // accumulator layout: lane l holds tile column l%16, rows 4*(l/16)+e
-    const int rbase = bm * 16 * RT + wm * 64 + 4 * (lane >> 4);
+    // Epilogue through LDS.  The accumulators hold, per lane, one column and
+    // four rows of each 16 x 16 tile, so stores straight from them write 2- or
+    // 4-byte pieces scattered over rows (measured on the 5000-token prefill:
+    // skipping every store of these kernels saved 8.5 of 126 ms).  Instead
+    // each wavefront writes its results into its own 16 KB region of the LDS
+    // ring (free once every wavefront has passed the last k-step) and copies
+    // them out in whole pieces: a SwiGLU output fragment (16 rows x 32
+    // features in operand order) as one contiguous 1 KB store of hi and one
+    // of lo, fp32 partial rows in pieces of SC / 4 lanes x 16 bytes.  The
+    // region is [64 rows][SC floats] (SC = 64, or 32 for the 64-row shape,
+    // whose ring is smaller) with the 16-byte column index XORed with the
+    // row, so the rows read by a fragment's lanes fall on distinct banks.
+    constexpr int SC = S::NW * 64 * 64 * 4 <= STAGES * STAGE * 2 ? 64 : 32;
+    static_assert(S::NW * 64 * SC * 4 <= STAGES * STAGE * 2 && 8 * JT <= SC, "epilogue staging fits in the LDS ring");
+    __syncthreads();
+    float *stg = reinterpret_cast<float *>(lds) + w * 64 * SC;
+    auto sidx = [](int r, int c) { return r * SC + ((((c >> 2) ^ r) & (SC / 4 - 1)) << 2) + (c & 3); };
+    const int lrow = 4 * (lane >> 4);  // accumulator layout: lane l holds tile column l%16, rows 4*(l/16)+e
+    const int row0 = bm * 16 * RT + wm * 64;  // the wavefront's first row
     if (EPI == EPI_SWIGLU) {
         // gate/up interleaved: column j < 8 of weight tile t is the gate of
         // feature 8t+j, column j+8 its up (lane l+8 holds it); the output is
         // the down projection's operand, in operand order
         bf16_t *A = (bf16_t *)a.out;
         bf16_t *Alo = (bf16_t *)a.out_lo;
+        constexpr int NFEAT = 8 * JT;  // features of the wavefront: 64 or 32
         const bool gate_lane = (lane & 8) == 0;
 #pragma unroll
-        for (int j = 0; j < JT; ++j) {
-            const int t = bn * WT + wn * JT + j;
-            const int f = 8 * t + (lane & 7);
+        for (int j = 0; j < JT; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float g = acc[i][j][e];
                     const float u = __shfl_xor(g, 8);
-                    const int r = rbase + i * 16 + e;
-                    if (gate_lane && t < ntiles && r < a.R) store_operand(A, Alo, perm_offset(r, f, a.N), silu_f(g) * u);
+                    if (gate_lane) stg[sidx(16 * i + lrow + e, 8 * j + (lane & 7))] = silu_f(g) * u;
                 }
-        }
-        return;
-    }
-    float *out = (float *)a.out + (size_t)sp * a.R * a.ldo;
-#pragma unroll
-    for (int j = 0; j < JT; ++j) {
-        const int t = bn * WT + wn * JT + j;
-        if (t >= ntiles) continue;
+        __syncthreads();
+        const int f_base = 8 * (bn * WT + wn * JT);  // a multiple of 32: k-step aligned
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = rbase + i * 16 + e;
-                if (r >= a.R) continue;
-                float *o = out + (size_t)r * a.ldo + t * 16 + (lane & 15);
-                if (EPI == EPI_RESID) *o += acc[i][j][e];
-                else *o = acc[i][j][e];
+            for (int ks = 0; ks < NFEAT / 32; ++ks) {
+                const int lr = 16 * i + (lane & 15), c = 32 * ks + 8 * (lane >> 4);
+                const int r = row0 + lr, f = f_base + c;
+                if (r >= a.R || f >= a.N) continue;
+                const f32x4 v0 = *reinterpret_cast<const f32x4 *>(&stg[sidx(lr, c)]);
+                const f32x4 v1 = *reinterpret_cast<const f32x4 *>(&stg[sidx(lr, c + 4)]);
+                const float y[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+                uint32_t hi[4], lo[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bf16_t h0 = f32_to_bf16(y[2 * q]), h1 = f32_to_bf16(y[2 * q + 1]);
+                    const bf16_t l0 = f32_to_bf16(y[2 * q] - bf16_to_f32(h0)), l1 = f32_to_bf16(y[2 * q + 1] - bf16_to_f32(h1));
+                    hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                    lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+                }
+                const size_t off = perm_offset(r, f, a.N);
+                *reinterpret_cast<u32x4 *>(A + off) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+                *reinterpret_cast<u32x4 *>(Alo + off) = u32x4{lo[0], lo[1], lo[2], lo[3]};
             }
+        return;
+    }
+    // fp32 rows [R][ldo], SC / 16 weight tiles (SC columns) at a time
+    constexpr int JC = SC / 16, LPR = SC / 4;  // tiles per pass, lanes per row
+    float *out = (float *)a.out + (size_t)sp * a.R * a.ldo;
+#pragma unroll
+    for (int j0 = 0; j0 < JT; j0 += JC) {
+        if (j0 > 0) __syncthreads();  // the previous pass's reads are done
+#pragma unroll
+        for (int j = 0; j < JC; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) stg[sidx(16 * i + lrow + e, 16 * j + (lane & 15))] = acc[i][j0 + j][e];
+        __syncthreads();
+        const int c = 4 * (lane % LPR);        // this lane's four columns of the SC
+        const int t = bn * WT + wn * JT + j0 + c / 16;
+#pragma unroll
+        for (int q = 0; q < 64 / (64 / LPR); ++q) {
+            const int lr = (64 / LPR) * q + lane / LPR;
+            const int r = row0 + lr;
+            if (r >= a.R || t >= ntiles) continue;
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(&stg[sidx(lr, c)]);
+            f32x4 *o = reinterpret_cast<f32x4 *>(out + (size_t)r * a.ldo + 16 * t + (c & 15));
+            if (EPI == EPI_RESID) *o += v;
+            else *o = v;
+        }
     }
 }
 
