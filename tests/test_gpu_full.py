@@ -4,7 +4,8 @@ benchmark times (one kvr_repair call over the whole position set).
 * Llama-3-8B shape (32 layers, d 4096, 32/8 heads x 128, FFN 14336, vocab
   128256), 5000-token context, 16-token edit at a seeded position in
   [1000, 4000], EditLocal K=32 (48 rows): every repaired output is compared
-  with the oracle.  Prefill at n=5000 is checked on its first 32 rows (which
+  with the oracle; and 128 rows at 4850-4977 with unsplit attention items
+  (the prefill's variant) over ~4900 keys.  Prefill at n=5000 is checked on its first 32 rows (which
   depend only on the first 32 tokens) and, at any size, by the endpoint
   property (repairing every position equals prefill).
 * Qwen2.5-7B shape (QKV bias, 28/4 heads): K in {8, 32, 128, 512} for both
@@ -78,6 +79,17 @@ def test_llama8b_repair_edit_local(llama):
     e = synth.edit_position(1000, 4000)
     A = osel.select_edit_local(N, e, e + SPAN, 32)
     _full_repair(llama, N, e, e + SPAN, A, tag=f"llama8b n=5000 edit@{e} EditLocal K=32")
+
+
+def test_llama8b_long_key_unsplit_attention(llama, monkeypatch):
+    """The prefill's attention variant (64-row items, one key group, every
+    key of the row block in one item) over ~4900 keys at full size: 128 rows
+    at the end of a 5000-token context, with the attention planner's target
+    forced so low that no key range is split."""
+    monkeypatch.setenv("KVR_ATT_TARGET", "1")
+    e = 4850
+    A = osel.select_edit_local(N, e, e + SPAN, 112)
+    _full_repair(llama, N, e, e + SPAN, A, tag=f"llama8b n=5000 edit@{e} EditLocal K=112, unsplit attention")
 
 
 def test_llama8b_prefill_prefix(llama):
