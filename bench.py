@@ -261,6 +261,16 @@ def main():
     pflops = prefill_flops(shape, plans)
     prefill_tflops = pflops / (prefill_ms * 1e-3) / 1e12
     log(f"prefill of every edited context: median {prefill_ms:.2f} ms, {prefill_tflops:.0f} TFLOP/s algorithmic")
+    libref = None
+    if not batched:
+        # one more prefill with the step profiler on: kernel time per step,
+        # set beside the vendor library's GEMM and attention at the same shapes
+        kvr.kvr_profile_enable(ctx, True)
+        kvr.kvr_profile_read(ctx)
+        prefill_all()
+        pprof = kvr.kvr_profile_read(ctx)
+        kvr.kvr_profile_enable(ctx, False)
+        libref = library_reference(torch, shape, plans[0][0], pprof)
     del pcache
 
     steps_ms = {k: round(v[0] / args.steps, 4) for k, v in prof.items() if v[1]}
@@ -365,8 +375,63 @@ def main():
         out["median_over_seeds_ms"] = round(statistics.median(per_seed), 4)
     if adj is not None:
         out["adjacent_rows"] = adj
+    if libref is not None:
+        out["prefill_vs_library"] = libref
     print(json.dumps(out), flush=True)
     kvr.kvr_destroy(ctx)
+
+
+def library_reference(torch, shape, n, pprof):
+    """The prefill's projections and attention beside the vendor library at the
+    same shapes.  Every product of the engine's compensated operand pairs is two
+    MFMAs, so the like-for-like library figure is torch.matmul (hipBLASLt) with
+    2n bf16 rows (the hi and lo halves stacked: the same issued MFMA work); the
+    n-row figure is a plain single-operand bf16 GEMM.  Attention is torch's
+    causal scaled_dot_product_attention over single bf16 operands, with the key
+    and value heads expanded to the query heads.  Times are µs per layer (the
+    engine's from its step profiler over one prefill)."""
+    dev = torch.device("cuda:0")
+    L, d, F = shape.n_layers, shape.d_model, shape.d_ffn
+    hd, hq, hkv = shape.head_dim, shape.n_heads, shape.n_kv_heads
+    s = torch.cuda.current_stream()
+
+    def t_us(fn, reps=10):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    def eng_us(step):
+        ms_, cnt = pprof.get(step, (0.0, 0))
+        return round(ms_ * 1e3 / L, 1) if cnt else None
+
+    out = {"rows": n, "library": f"torch {torch.__version__} matmul / scaled_dot_product_attention, bf16"}
+    gemms = {"qkv_proj": (d, (hq + 2 * hkv) * hd), "o_proj": (hq * hd, d),
+             "gate_up_swiglu": (d, 2 * F), "down_proj": (F, d)}
+    for step, (K, N) in gemms.items():
+        w = torch.randn(N, K, device=dev, dtype=torch.bfloat16)
+        a = torch.randn(2 * n, K, device=dev, dtype=torch.bfloat16)
+        lib2 = t_us(lambda: torch.matmul(a, w.t()))
+        a1 = a[:n]
+        lib1 = t_us(lambda: torch.matmul(a1, w.t()))
+        del a, a1, w
+        e = eng_us(step)
+        out[step] = {"engine_us": e, "library_us_2n_rows": round(lib2, 1), "library_us_n_rows": round(lib1, 1),
+                     "engine_tflops_algorithmic": round(2 * n * N * K / (e * 1e-6) / 1e12, 1) if e else None}
+    q = torch.randn(1, hq, n, hd, device=dev, dtype=torch.bfloat16)
+    k = torch.randn(1, hkv, n, hd, device=dev, dtype=torch.bfloat16).repeat_interleave(hq // hkv, dim=1)
+    v = torch.randn(1, hkv, n, hd, device=dev, dtype=torch.bfloat16).repeat_interleave(hq // hkv, dim=1)
+    lib = t_us(lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True))
+    del q, k, v
+    e = eng_us("attention")
+    out["attention"] = {"engine_us": e, "library_us": round(lib, 1)}
+    log(f"prefill vs library (us per layer): {out}")
+    return out
 
 
 ADJ_SLOTS = 64     # cache slots past the context for appended query/answer tokens
