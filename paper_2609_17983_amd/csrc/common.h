@@ -135,6 +135,12 @@ struct LinearArgs {
                           // tiles out[s][R][ldo] summed by the consumer (<= 1: none)
     int32_t group_all;    // tiled: at most this many row blocks form one group of the tile order (set by the launcher)
     int32_t tpb;          // tall kernel: weight tiles per block (0: not the tall kernel)
+    // tall kernel: RMS scale of the rows (resid_gain), as in SkinnyArgs: when
+    // rs_ssq is set, output row r is multiplied by
+    // rsqrt((rs_ssq[0][r] + ... + rs_ssq[rs_nb-1][r]) / rs_d + rs_eps)
+    const float *rs_ssq;
+    int32_t rs_nb, rs_d;
+    float rs_eps;
 };
 
 // Skinny (R <= 64) linear layer: X in operand order, W packed in operand order

@@ -422,6 +422,20 @@ void plan_packed(const kvr_ctx *c, LinearArgs &a, int epi) {
     if (epi == EPI_STORE) a.split = tiled_split(c, a.R, vrows, a.K);
 }
 
+// A tall projection reading the RMSNorm output applies the RMS scale to its
+// output rows, as the skinny kernels do: the residual step then runs over
+// (row, column block) blocks (resid_gain) instead of one block per row, whose
+// 144 blocks at 144 rows leave compute units idle while they sum the output
+// projection's partial tiles.  KVR_TALL_ROWSCALE=0 keeps the per-row kernel.
+bool tall_row_scale(const LinearArgs &a) { return a.tpb > 0 && a.x_lo && env_int("KVR_TALL_ROWSCALE", 1) != 0; }
+
+void set_row_scale(LinearArgs &a, const float *ssq, int K, float eps) {
+    a.rs_ssq = ssq;
+    a.rs_nb = resid_gain_blocks(K);
+    a.rs_d = K;
+    a.rs_eps = eps;
+}
+
 // Step profiler: arm() hands two events to the next kernel launch, which
 // records them around its execution; disarm() files them under `step` (or
 // returns them when the launcher enqueued nothing).
@@ -531,8 +545,17 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
     for (int l = 0; l < n_run; ++l) {
         const kvr_layer_weights &w = c->layers[l];
         const kvr_ctx::PackedLayer pw = c->wpk ? c->pk[l] : kvr_ctx::PackedLayer{nullptr, nullptr, nullptr, nullptr};
-        // skinny passes: the projections apply the RMS scale to their outputs
-        if (sk)
+        // skinny and tall passes: the projections apply the RMS scale to their
+        // outputs (resid_gain spreads the residual step over column blocks)
+        LinearArgs qa{};
+        bool rg = sk;
+        if (!sk) {
+            qa = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr, NQKV);
+            qa.grp = c->qkv_grp;
+            plan_packed(c, qa, EPI_STORE);
+            rg = tall_row_scale(qa);
+        }
+        if (rg)
             KVR_CHECK(launch_resid_gain(bf, c->H, c->P, resid_split, w.attn_norm, R, D, c->Xn, c->Xn_lo, c->rs_ssq, s),
                       "rmsnorm(attn)", ST_NORM);
         else
@@ -546,12 +569,9 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                       "qkv", ST_QKV);
             qkv_split = p_qkv.split;
         } else {
-            LinearArgs a = make_args(c->Xn, c->Xn_lo, D, R, D, NQKV, w.wq, w.wk, w.wv, qd, qd + kd, pw.qkv, c->P, nullptr,
-                                     NQKV);
-            a.grp = c->qkv_grp;
-            plan_packed(c, a, EPI_STORE);
-            KVR_CHECK(linear(c, EPI_STORE, a, s), "qkv", ST_QKV);
-            qkv_split = a.split;
+            if (rg) set_row_scale(qa, c->rs_ssq, D, d.rms_eps);
+            KVR_CHECK(linear(c, EPI_STORE, qa, s), "qkv", ST_QKV);
+            qkv_split = qa.split;
         }
         KVR_CHECK(launch_rope_scatter(bf, c->P, qkv_split, w.bq, w.bk, w.bv, rows, docs, R, l, d.n_heads, d.n_kv_heads,
                                       hd, c->rope_cos, c->rope_sin, c->Qb, c->Qb_lo, s), "rope_scatter", ST_ROPE);
@@ -590,7 +610,15 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
             KVR_CHECK(linear(c, EPI_RESID, make_args(c->Ob, c->Ob_lo, qd, R, qd, D, w.wo, w.wo, w.wo, D, D, pw.o, c->H, nullptr, D), s),
                       "o_proj", ST_OPROJ);
         }
-        if (sk)
+        LinearArgs ga{};
+        rg = sk;
+        if (!sk) {
+            ga = make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu, c->Ab, c->Ab_lo, F);
+            ga.grp = c->gu_grp;
+            plan_packed(c, ga, EPI_SWIGLU);
+            rg = tall_row_scale(ga);
+        }
+        if (rg)
             KVR_CHECK(launch_resid_gain(bf, c->H, c->P, resid_split, w.mlp_norm, R, D, c->Xn, c->Xn_lo, c->rs_ssq, s),
                       "rmsnorm(mlp)", ST_NORM);
         else
@@ -606,10 +634,7 @@ kvr_status run_pass(kvr_ctx *c, Tables &t, hipStream_t s, int kv_layer = -1, con
                       ST_DOWN);
             resid_split = p_down.split;
         } else {
-            LinearArgs ga = make_args(c->Xn, c->Xn_lo, D, R, D, F, w.w_gate, w.w_up, w.w_up, F, F, pw.gu, c->Ab,
-                                      c->Ab_lo, F);
-            ga.grp = c->gu_grp;
-            plan_packed(c, ga, EPI_SWIGLU);
+            if (rg) set_row_scale(ga, c->rs_ssq, D, d.rms_eps);
             if (ga.tpb > 0 && ga.split > 1) {
                 // split gate/up (tall): fp32 partials of the 2F interleaved
                 // columns into P (free: the residual step consumed the output
@@ -823,7 +848,7 @@ kvr_status kvr_create(const kvr_dims *dims, const kvr_weights *wts, kvr_ctx **ou
                  o_Al = take(R * F * lo_es),
                  o_cos = take((size_t)d.max_ctx * (hd / 2) * 4), o_sin = take((size_t)d.max_ctx * (hd / 2) * 4),
                  o_ap = take(c->attn_part_floats * 4), o_tab = take(c->tables_bytes),
-                 o_ss = take((size_t)64 * resid_gain_blocks(D) * 4);
+                 o_ss = take(std::max<size_t>(64, tall_rows) * resid_gain_blocks(D) * 4);
     c->ws_bytes = off;
     e = hipMalloc((void **)&c->ws, c->ws_bytes);
     if (e != hipSuccess) { delete c; return fail(nullptr, KVR_E_NOMEM, "kvr_create: workspace allocation failed"); }

@@ -147,6 +147,16 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
 #pragma unroll
         for (int j = 0; j < NTW; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // row threadIdx.x's sums of squares (the first four column blocks),
+    // loaded before the ring starts and first used in the epilogue
+    const bool rs_row = a.rs_ssq && (int)threadIdx.x < a.R;
+    float rs_pre[4] = {0.f, 0.f, 0.f, 0.f};
+    if (rs_row) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (q < a.rs_nb) rs_pre[q] = a.rs_ssq[(size_t)q * a.R + threadIdx.x];
+    }
+
     for (int j = 0; j < STAGES - 1 && j < nk; ++j) issue();
     for (int kk = 0; kk < nk; ++kk) {
         // k-step kk's fragments (this wavefront's) have landed: the k-steps
@@ -178,8 +188,33 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
     bool tv[NTW];  // weight tile w + 4 j of the block exists
 #pragma unroll
     for (int j = 0; j < NTW; ++j) tv[j] = t0 + w + 4 * j < tend;
+    if (a.rs_ssq) {
+        // RMS scales of the rows (the sums in column-block order, as the
+        // skinny kernel takes them), handed over through LDS: the ring is no
+        // longer read after the first barrier
+        float *rsl = reinterpret_cast<float *>(lds);
+        float sc = 1.f;
+        if (rs_row) {
+            float t = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (q < a.rs_nb) t += rs_pre[q];
+            for (int b = 4; b < a.rs_nb; ++b) t += a.rs_ssq[(size_t)b * a.R + threadIdx.x];
+            sc = rsqrtf(t / (float)a.rs_d + a.rs_eps);
+        }
+        __syncthreads();
+        if ((int)threadIdx.x < 16 * MT) rsl[threadIdx.x] = sc;
+        __syncthreads();
+    }
     // accumulator layout: lane l holds tile column l%16, rows 16 m + 4 (l/16) + e
     const int rq = 4 * (lane >> 4);
+    // the scale of each of this lane's rows (1 without rs_ssq), applied as
+    // the accumulators are stored
+    float rsc[MT][4];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rsc[m][e] = a.rs_ssq ? reinterpret_cast<const float *>(lds)[16 * m + rq + e] : 1.f;
     if (EPI == EPI_SWIGLU) {
         // column c < 8 of tile t is the gate of feature 8t + c, column c + 8
         // its up (held by lane l + 8)
@@ -194,8 +229,8 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float g = acc[m][j][e];
-                    const float u = __shfl_xor(g, 8);
+                    const float g = acc[m][j][e] * rsc[m][e];
+                    const float u = __shfl_xor(g, 8);  // lane l + 8: the same row
                     const int r = 16 * m + rq + e;
                     if (gate_lane && r < a.R) store_operand(A, Alo, perm_offset(r, f, a.N), silu_f(g) * u);
                 }
@@ -212,7 +247,7 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int r = 16 * m + rq + e;
-                if (r < a.R) out[(size_t)r * a.ldo + c] = acc[m][j][e];
+                if (r < a.R) out[(size_t)r * a.ldo + c] = acc[m][j][e] * rsc[m][e];
             }
     }
 }

@@ -471,16 +471,18 @@ def test_mid_tall_rows(mid, rows, policy):
 # that do not divide its k-steps, blocks of more than 12 tiles (five per
 # wavefront), the gate/up projection fused with its SwiGLU or split in two
 # (partials finished by the SwiGLU pass; the default plan at these sizes),
-# and the tiled kernel for the same rows.
+# the tiled kernel for the same rows, and the per-row RMSNorm kernel in place
+# of the residual step by column blocks with the RMS scale applied by the
+# projections.
 TALL_OVERRIDES = [{"KVR_TALL_TPB": "5", "KVR_TALL_SPLIT": "3"}, {"KVR_TALL_TPB": "1", "KVR_TALL_SPLIT": "7"},
                   {"KVR_TALL_TPB": "12", "KVR_TALL_SPLIT": "1", "KVR_TALL_GU_SPLIT": "1"},
                   {"KVR_TALL_TPB": "17", "KVR_TALL_SPLIT": "2"},
                   {"KVR_TALL_TPB": "20", "KVR_TALL_SPLIT": "1", "KVR_TALL_GU_SPLIT": "2"},
-                  {"KVR_TALL_GU_SPLIT": "1"}, {"KVR_TALL": "0"}]
+                  {"KVR_TALL_GU_SPLIT": "1"}, {"KVR_TALL": "0"}, {"KVR_TALL_ROWSCALE": "0"}]
 
 
 @pytest.mark.parametrize("env", TALL_OVERRIDES, ids=["tpb5-split3", "tpb1-split7", "tpb12-unsplit", "tpb17-split2",
-                                                     "tpb20-gu-split2", "fused-swiglu", "tiled"])
+                                                     "tpb20-gu-split2", "fused-swiglu", "tiled", "per-row-norm"])
 def test_mid_tall_plan_overrides(mid, monkeypatch, env):
     shape, eng, ow, toks, new, stale_np = mid
     for k, v in env.items():
