@@ -148,7 +148,8 @@ __global__ __launch_bounds__(256, 1) void linear_tall_kernel(LinearArgs a) {
         for (int j = 0; j < NTW; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // row threadIdx.x's sums of squares (the first four column blocks),
-    // loaded before the ring starts and first used in the epilogue
+    // loaded before the ring starts and first used in the epilogue; they are
+    // older than every ring load, so the ring's exact waits cover them too
     const bool rs_row = a.rs_ssq && (int)threadIdx.x < a.R;
     float rs_pre[4] = {0.f, 0.f, 0.f, 0.f};
     if (rs_row) {
