@@ -288,7 +288,8 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
 // block streams NT tiles over its K slice, and blocks beyond one per compute
 // unit run in a further round.  The plan minimises
 //   rounds * NT * k-steps per slice,   rounds = ceil(blocks / 256),
-// over NT <= 8 (7 for 64 rows, whose accumulators would spill at 8) and
+// over NT <= 10 (7 for 64 rows, whose accumulators would spill at 8 and
+// whose wavefronts' partial sums would not fit in LDS beyond 8) and
 // splits up to the largest power of two that keeps each wavefront's K slice
 // above `wave_ks` k-steps (and at least 7, which lets the Qwen2.5-7B output
 // projection's 112 k-steps take 4 x 4: 0.312 -> 0.293 ms per repair), never
@@ -297,8 +298,10 @@ void plan_attention(const kvr_ctx *c, Tables &t) {
 // projection and the LM head and 8 for the output and down projections.
 // Measured on the 8B shape this reproduces the best of the swept plans
 // (QKV 3 x 2, O 4 x 4, gate/up 7, down 8 x 8); on the Qwen2.5-7B shape it
-// takes gate/up 5 (474 blocks; 67 us against 77-85 us at 8) and down 7 x 8
-// (32 us against 43 us at 8 x 16).
+// takes gate/up 10 (237 blocks in one round, tied with 5 in two rounds of
+// 474: each block reads the whole activation matrix from L2, so the wider
+// block halves that traffic; 48 rows: 1.70 -> 1.45 ms per repair, against
+// 2.12 ms at 8, 296 blocks) and down 7 x 8 (32 us against 43 us at 8 x 16).
 struct SkinnyPlan { int nt, split; };
 
 SkinnyPlan plan_skinny(int ntiles, int K, int R, bool swiglu, int wave_ks, const char *env_nt,
@@ -307,7 +310,7 @@ SkinnyPlan plan_skinny(int ntiles, int K, int R, bool swiglu, int wave_ks, const
     int smax = 1;
     if (!swiglu)
         while (smax * 2 <= SPLIT_MAX && ksteps / (4 * smax) > wave_ks && ksteps / (8 * smax) >= 7) smax *= 2;
-    const int ntmax = (R + 15) / 16 >= 4 ? 7 : 8;
+    const int ntmax = (R + 15) / 16 >= 4 ? 7 : 10;
     SkinnyPlan p{1, 1};
     long long best = -1;
     for (int sp = 1; sp <= smax; sp *= 2)
@@ -322,7 +325,7 @@ SkinnyPlan plan_skinny(int ntiles, int K, int R, bool swiglu, int wave_ks, const
     const int es = env_split ? env_int(env_split, 0) : 0;
     if (!swiglu && es >= 1) p.split = std::min(es, std::min(SPLIT_MAX, ksteps));
     const int nt = env_int(env_nt, 0);
-    if (nt >= 1 && nt <= 8) p.nt = nt;
+    if (nt >= 1 && nt <= ((R + 15) / 16 <= 3 ? 10 : 8)) p.nt = nt;
     return p;
 }
 

@@ -246,6 +246,18 @@ hipError_t launch_nt(int epi, const SkinnyArgs &a, hipStream_t s) {
     }
 }
 
+// Blocks of more than eight tiles: at most 48 rows (the wavefronts' partial
+// sums of 64 rows would not fit in LDS).
+template <int NT>
+hipError_t launch_nt_wide(int epi, const SkinnyArgs &a, hipStream_t s) {
+    switch ((a.R + 15) / 16) {
+        case 1: return launch_mt_nt<1, NT>(epi, a, s);
+        case 2: return launch_mt_nt<2, NT>(epi, a, s);
+        case 3: return launch_mt_nt<3, NT>(epi, a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_t s) {
@@ -268,6 +280,8 @@ hipError_t launch_linear_skinny(int epi, const SkinnyArgs &a, int nt, hipStream_
         case 6: return launch_nt<6>(epi, a, s);
         case 7: return launch_nt<7>(epi, a, s);
         case 8: return launch_nt<8>(epi, a, s);
+        case 9: return launch_nt_wide<9>(epi, a, s);
+        case 10: return launch_nt_wide<10>(epi, a, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -422,10 +422,13 @@ PLAN_OVERRIDES = [
      "KVR_NT_DOWN": "7", "KVR_SPLIT_DOWN": "4"},
     {"KVR_NT_QKV": "8", "KVR_SPLIT_QKV": "4", "KVR_NT_O": "8", "KVR_SPLIT_O": "2", "KVR_NT_GATEUP": "6",
      "KVR_NT_DOWN": "8", "KVR_SPLIT_DOWN": "8"},
+    # blocks of nine and ten tiles (passes of at most 48 rows), ragged last blocks
+    {"KVR_NT_QKV": "9", "KVR_SPLIT_QKV": "2", "KVR_NT_O": "10", "KVR_SPLIT_O": "4", "KVR_NT_GATEUP": "10",
+     "KVR_NT_DOWN": "9", "KVR_SPLIT_DOWN": "3"},
 ]
 
 
-@pytest.mark.parametrize("env", PLAN_OVERRIDES, ids=["nt1-2-3", "nt4-5-6-7", "nt6-8"])
+@pytest.mark.parametrize("env", PLAN_OVERRIDES, ids=["nt1-2-3", "nt4-5-6-7", "nt6-8", "nt9-10"])
 def test_mid_skinny_plan_overrides(mid, monkeypatch, env):
     shape, eng, ow, toks, new, stale_np = mid
     for k, v in env.items():
