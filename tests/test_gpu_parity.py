@@ -273,6 +273,39 @@ def test_mid_repair(mid, policy, K):
     _repair_case(shape, eng, ow, stale_np, new, 300, 316, A, f"mid {policy} K={K}", n_cap=704)
 
 
+# Seeded sweep over edit placements, span lengths, budgets and both policies,
+# so that one run covers every projection kernel (skinny up to 64 rows, tall to
+# 192, tiled above), split and unsplit attention items, and the pool's edges:
+# an edit at position 0, an edit that ends at the last position (empty pool),
+# a budget larger than the pool.
+def _sweep_cases():
+    rng = np.random.default_rng(2609)
+    cases = [(0, 8, 32, "edit_local", 0), (690, 9, 0, "edit_local", 0), (640, 4, 500, "random", 11),
+             (100, 16, 250, "random", 5), (50, 24, 400, "edit_local", 0)]
+    for i in range(9):
+        span = int(rng.integers(1, 25))
+        s0 = int(rng.integers(0, 700 - span))
+        K = int(rng.choice([1, 5, 17, 40, 63, 100, 150, 250]))
+        policy = "edit_local" if i % 2 == 0 else "random"
+        cases.append((s0, span, K, policy, int(rng.integers(0, 1 << 30))))
+    return cases
+
+
+SWEEP = _sweep_cases()
+
+
+@pytest.mark.parametrize("s0,span,K,policy,seed", SWEEP,
+                         ids=[f"{p}-e{s}+{n}-K{k}" for s, n, k, p, _ in SWEEP])
+def test_mid_repair_sweep(mid, s0, span, K, policy, seed):
+    shape, eng, ow, toks, _, stale_np = mid
+    n, s1 = 700, s0 + span
+    new_i = synth.apply_edit(toks, s0, span, shape.vocab, label=seed & 0xffff)
+    A = (osel.select_edit_local(n, s0, s1, K) if policy == "edit_local"
+         else osel.select_random(n, s0, s1, K, seed))
+    _repair_case(shape, eng, ow, stale_np, new_i, s0, s1, A,
+                 f"mid sweep {policy} edit [{s0},{s1}) K={K} ({span + len(A)} rows)", n_cap=704)
+
+
 def test_mid_repair_is_idempotent_and_deterministic(mid):
     shape, eng, ow, toks, new, stale_np = mid
     cache = torch.from_numpy(stale_np).to(torch.bfloat16).cuda()
