@@ -270,7 +270,11 @@ def main():
         prefill_all()
         pprof = kvr.kvr_profile_read(ctx)
         kvr.kvr_profile_enable(ctx, False)
-        libref = library_reference(torch, shape, plans[0][0], pprof)
+        try:
+            libref = library_reference(torch, shape, plans[0][0], pprof)
+        except Exception as ex:  # the reference leg never costs the bench line
+            libref = {"error": f"{type(ex).__name__}: {ex}"}
+            log(f"library reference skipped: {libref['error']}")
     del pcache
 
     steps_ms = {k: round(v[0] / args.steps, 4) for k, v in prof.items() if v[1]}
